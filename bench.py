@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Throughput of the DP-SGD clipped + noised gradient step on one MI355X.
+
+One step is the whole GPU-side path of the paper's DP-SGD step over one batch:
+per-example norms of every layer (one global norm per example), clip factors,
+the clip-weighted sum of every layer, and Philox/Box-Muller noise added to
+every sum -- three C-ABI calls. Inputs (captured activations and output
+gradients of every linear layer) are synthetic, seeded, drawn on the GPU and
+resident in HBM before timing starts.
+
+Prints one JSON line. ``value`` is examples/s of whole steps; ``roofline``
+reports the dominant kernel (the clip-weighted sum, an MFMA contraction)
+against the bf16 dense MFMA peak; ``cpu_baseline`` is the float64 oracle timed
+on this host on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+if HERE not in sys.path:
+    sys.path.insert(0, HERE)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+METRIC = "DP-SGD clipped+noised grad throughput: examples/s per layer; % MFMA peak"
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-examples", type=int, default=4)
+    return p.parse_args()
+
+
+def algorithmic_work(W, mode_forms):
+    """FLOPs and bytes the method must do per step (not the dense work it avoids)."""
+    B, T = W.B, W.T
+    isz = 2 if W.dtype == "bf16" else 4
+    norm_flops = 0.0
+    clip_flops = 0.0
+    in_bytes = 0.0
+    noise_elems = 0
+    seen_a = set()
+    for l, s in enumerate(W.layers):
+        form = mode_forms[l]
+        if form == "t1":
+            norm_flops += 2.0 * B * (s.d_in + s.d_out)
+        elif form == "ghost":
+            norm_flops += float(B) * T * (T + 1) * (s.d_in + s.d_out)
+        else:
+            norm_flops += 2.0 * B * T * s.d_in * s.d_out
+        clip_flops += 2.0 * B * T * s.d_in * s.d_out
+        key = s.share_a_with if s.share_a_with is not None else l
+        if key not in seen_a:
+            seen_a.add(key)
+            in_bytes += B * T * s.d_in * isz
+        in_bytes += B * T * s.d_out * isz
+        noise_elems += s.d_in * s.d_out
+    return dict(norm_flops=norm_flops, clip_flops=clip_flops, input_bytes=in_bytes,
+                clip_bytes=in_bytes + 4.0 * noise_elems, noise_bytes=8.0 * noise_elems,
+                noise_elems=noise_elems)
+
+
+def cpu_baseline(W, dev_layers, n_examples: int):
+    """The float64 oracle on this host: a few examples of every layer plus the
+    step's noise, scaled to examples/s of a whole B-example step."""
+    import torch
+    import oracle
+    from oracle import OracleLayer
+
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        blas_threads = None
+    b = min(n_examples, W.B)
+    layers = []
+    for d in dev_layers:
+        A = d["A"][:b].to("cpu", torch.float32).numpy().astype(np.float64)
+        G = d["G"][:b].to("cpu", torch.float32).numpy().astype(np.float64)
+        layers.append(OracleLayer(A, G, d["tensor_id"]))
+    t0 = time.perf_counter()
+    nsq = oracle.per_example_norms_sq(layers)
+    _, c, _ = oracle.clip_factors(nsq, W.C)
+    sums = [oracle.clipped_sum(L, c) for L in layers]
+    t1 = time.perf_counter()
+    for L, S in zip(layers, sums):
+        oracle.add_noise(S, W.sigma, W.C, W.noise_seed, L.tensor_id, W.step, 1.0 / W.B)
+    t2 = time.perf_counter()
+    per_example = (t1 - t0) / b
+    step_time = per_example * W.B + (t2 - t1)
+    cores = len(os.sched_getaffinity(0))
+    return {
+        "value": W.B / step_time,
+        "unit": "examples/s",
+        "cores": int(blas_threads) if blas_threads else cores,
+        "kind": "oracle",
+        "sample": (f"float64 oracle on {b} of {W.B} examples x {len(layers)} layers "
+                   f"(materialised per-example gradients, norms, clip, clipped sum: "
+                   f"{t1 - t0:.2f} s) plus the whole step's noise ({t2 - t1:.2f} s); "
+                   f"scaled to a {W.B}-example step; host cpus {cores}"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2609_20532_amd import dpsgd, workloads as wl
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    dpsgd.load()
+    W = wl.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layers_t = wl.make_layers_torch(W, dev)
+    Ls = [dpsgd.make_layer(d["A"], d["G"], d["tensor_id"]) for d in layers_t]
+    buf = dpsgd.alloc_step(Ls)
+    forms = []
+    for L in Ls:
+        if L.T == 1:
+            forms.append("t1")
+        else:
+            forms.append("ghost" if dpsgd.dpsgd_select_norm_mode(L) == dpsgd.DPSGD_NORM_GHOST
+                         else "mat")
+    work = algorithmic_work(W, forms)
+    scale = 1.0 / W.B
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        dpsgd.dpsgd_per_example_norms_multi(Ls, dpsgd.DPSGD_NORM_AUTO, buf.norms_sq,
+                                            workspace=buf.norms_ws)
+        if ev is not None:
+            ev[1].record()
+        dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads,
+                                          factors_out=buf.factors, mask_out=buf.mask,
+                                          workspace=buf.clip_ws)
+        if ev is not None:
+            ev[2].record()
+        dpsgd.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    t_norm = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    t_clip = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    t_noise = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+
+    mfma_peak = PEAK_BF16_TFLOPS if W.dtype == "bf16" else PEAK_FP32_TFLOPS
+    clip_tflops = work["clip_flops"] / (t_clip * 1e-3) / 1e12
+    norm_tflops = work["norm_flops"] / (t_norm * 1e-3) / 1e12
+    noise_gbs = work["noise_bytes"] / (t_noise * 1e-3) / 1e9
+    value = W.B / (ms_per_step * 1e-3)
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "examples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": W.dtype,
+        "data": "synthetic (seeded, drawn on the GPU; shapes and distributions of the workload)",
+        "config": {
+            "workload": f"{W.name}: {W.description}",
+            "B": W.B, "T": W.T, "layers": W.n_layers,
+            "layer_dims": sorted({(s.d_in, s.d_out) for s in W.layers}),
+            "C": W.C, "sigma": W.sigma, "noise_seed": W.noise_seed,
+        },
+        "examples_per_s_per_layer": value * W.n_layers,
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "clip-weighted sum (tgemm_kernel)",
+            "achieved": clip_tflops,
+            "peak": mfma_peak,
+            "unit": "TFLOP/s",
+            "frac": clip_tflops / mfma_peak,
+            "traffic": None,
+        },
+        "kernels": {
+            "norms_ms": t_norm, "norms_tflops": norm_tflops,
+            "norms_frac_mfma": norm_tflops / mfma_peak,
+            "clip_ms": t_clip, "clip_tflops": clip_tflops,
+            "noise_ms": t_noise, "noise_gbs": noise_gbs, "noise_frac_hbm": noise_gbs / PEAK_HBM_GBS,
+            "norm_forms": {f: forms.count(f) for f in set(forms)},
+            "algorithmic": work,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(W, layers_t, args.cpu_sample_examples)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * dpsgd.h -- C ABI of the MI355X (gfx950) DP-SGD gradient-step library.
+ *
+ * The library computes, on one GPU, the part of a DP-SGD step that the
+ * paper's protocol gives to the untrusted GPU (the algorithm "GPU-side
+ * Gradient Computation and Local Update" and Section 2.2, "DP-SGD"):
+ *
+ *   per-example gradient of each linear layer   g_i = G_i^T A_i
+ *   per-example L2 norm over all layers        n_i = sqrt(sum_l ||g_{i,l}||_F^2)
+ *   clip factor                                 c_i = min(1, C / n_i)
+ *   clipped sum over the batch                  S_l = sum_i c_i g_{i,l}
+ *   Gaussian noise of scale sigma*C             out = scale * (S_l + sigma*C*z)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - A linear layer y_t = W x_t is described by a dpsgd_layer: the
+ *    activations A [B][T][d_in] and output gradients G [B][T][d_out]
+ *    (G[i][t] = dloss_i/dy_t), both row-major and contiguous, both of the
+ *    same element type (float32 or bfloat16).
+ *  - Gradient-shaped buffers are float32 [d_out][d_in], row-major (the layout
+ *    of W itself).
+ *  - Every pointer to tensor data is a DEVICE pointer owned by the caller.
+ *    The library allocates no device memory, keeps no pointer after a call
+ *    returns and holds no mutable global state; calls are thread-safe.
+ *  - Arrays of descriptors (dpsgd_layer*, float* const*) are HOST memory and
+ *    are read before the call returns.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every call only enqueues kernels on it and returns; results are valid
+ *    once the caller synchronises with the stream. Faults inside a kernel
+ *    surface at that synchronisation.
+ *  - Every entry point returns a dpsgd_status. Nothing aborts or throws across
+ *    the ABI. On an error return nothing has been enqueued.
+ *  - Results are deterministic: the same inputs on the same device give
+ *    bitwise-identical outputs (no floating-point atomics).
+ *  - Arithmetic: products of bf16 inputs are exact in float32 and all sums
+ *    accumulate in float32.
+ */
+#ifndef DPSGD_H_
+#define DPSGD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dpsgd_dtype {
+  DPSGD_F32 = 0,   /* IEEE binary32                               */
+  DPSGD_BF16 = 1   /* bfloat16 (upper 16 bits of a binary32)       */
+} dpsgd_dtype;
+
+typedef enum dpsgd_norm_mode {
+  DPSGD_NORM_AUTO = 0,         /* pick per layer by arithmetic cost           */
+  DPSGD_NORM_GHOST = 1,        /* Gram form: sum_{t,s} (a_t.a_s)(g_t.g_s)     */
+  DPSGD_NORM_MATERIALIZE = 2   /* ||G_i^T A_i||_F^2, tile kept in registers   */
+} dpsgd_norm_mode;
+
+typedef enum dpsgd_status {
+  DPSGD_OK = 0,
+  DPSGD_ERR_INVALID_ARG = -1,  /* null required pointer, size < 1 or overflow, C <= 0 or NaN,
+                                  sigma < 0 or NaN, scale not finite                      */
+  DPSGD_ERR_UNSUPPORTED = -2,  /* unknown dtype or mode, mixed dtypes in one call         */
+  DPSGD_ERR_WORKSPACE = -3,    /* workspace NULL or smaller than the *_workspace_bytes value */
+  DPSGD_ERR_HIP = -4           /* the HIP runtime rejected a launch                       */
+} dpsgd_status;
+
+/* One linear layer y = x W^T (W: [d_out][d_in]) as seen by one batch.
+ * Paper: Section 2.2, per-example gradient of the trainable parameters. */
+typedef struct dpsgd_layer {
+  const void* A;       /* [B][T][d_in]  activations, dtype                       */
+  const void* G;       /* [B][T][d_out] output gradients dloss_i/dy_t, dtype     */
+  int64_t B;           /* examples in the batch, >= 1                            */
+  int64_t T;           /* positions per example (sequence length), >= 1          */
+  int64_t d_in;        /* >= 1                                                   */
+  int64_t d_out;       /* >= 1                                                   */
+  int32_t dtype;       /* dpsgd_dtype, shared by A and G                         */
+  uint32_t tensor_id;  /* third Philox counter word of this layer's noise        */
+} dpsgd_layer;
+
+/* ---------------------------------------------------------------------------
+ * Per-example norms.  Paper: Section 2.2 (per-example clipping uses
+ * ||g_t(x_i)||_2 over all trainable parameters); GPU-side algorithm, clip step.
+ *
+ * norms_sq[i] = (accumulate ? norms_sq[i] : 0) + sum_l ||G_{l,i}^T A_{l,i}||_F^2
+ *
+ * over the n_layers layers of the call, all with the same B. One call over all
+ * layers of a step gives the squared global norm; per-layer calls with
+ * accumulate=1 give the same value up to float32 summation order.
+ *   mode      dpsgd_norm_mode, applied to every layer (AUTO picks per layer).
+ *   norms_sq  float32 [B], device.
+ *   workspace device scratch of at least dpsgd_norms_workspace_bytes(...)
+ *             bytes (may be NULL when that value is 0); its contents on entry
+ *             do not matter and are clobbered.
+ * T = 1 layers always use the closed form ||a||^2 ||g||^2 whatever the mode.
+ * ------------------------------------------------------------------------- */
+size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode);
+
+/* The form AUTO selects for this layer (DPSGD_NORM_GHOST or _MATERIALIZE),
+ * or a negative dpsgd_status for an invalid descriptor. */
+int32_t dpsgd_select_norm_mode(const dpsgd_layer* layer);
+
+int dpsgd_per_example_norms(const dpsgd_layer* layer, int32_t mode, float* norms_sq,
+                            int32_t accumulate, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode,
+                                  float* norms_sq, int32_t accumulate, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Clip factors.  Paper: Section 2.2, g_bar_i = g_i * min(1, C/||g_i||_2).
+ *
+ *   n_i = sqrt(norms_sq[i]);  factors[i] = n_i > C ? C / n_i : 1;
+ *   mask[i] = n_i > C          (1 = clipped; a tie n_i == C is not clipped)
+ * computed in float32. C must be > 0 (C = +inf disables clipping).
+ * factors (float32 [B]) and mask (uint8 [B]) are device pointers; either may be NULL.
+ * ------------------------------------------------------------------------- */
+int dpsgd_clip_factors(const float* norms_sq, int64_t B, float C, float* factors,
+                       uint8_t* mask, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Clipped sum.  Paper: Section 2.2 aggregation sum_i g_bar_i; GPU-side
+ * algorithm, average step (the 1/B is left to dpsgd_add_noise's `scale`).
+ *
+ *   grad = (accumulate ? grad : 0) + sum_i c_i G_i^T A_i      (float32 [d_out][d_in])
+ *
+ * with c_i from dpsgd_clip_factors(norms_sq, B, C). factors_out / mask_out
+ * (device, optional) receive c and the clip mask. The _multi form does the
+ * same for n_layers layers (one grad buffer each, all with the same B) in one
+ * grouped launch. workspace: at least dpsgd_clip_workspace_bytes(...) bytes.
+ * grad must not alias any input.
+ * ------------------------------------------------------------------------- */
+size_t dpsgd_clip_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers);
+
+int dpsgd_clip_accumulate(const dpsgd_layer* layer, const float* norms_sq, float C,
+                          float* grad, int32_t accumulate, float* factors_out,
+                          uint8_t* mask_out, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
+                                const float* norms_sq, float C, float* const* grads,
+                                int32_t accumulate, float* factors_out, uint8_t* mask_out,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Noise.  Paper: Section 2.2, z_t ~ N(0, sigma^2 C^2 I) and
+ * g_tilde = (1/|B_t|)(sum + z_t); GPU-side algorithm, noise step
+ * (g_tilde = g_bar + Noise(s_noise,t; sigma C)/B).
+ *
+ *   grad[e] = scale * (grad[e] + sigma * C * z_e),   e in [0, d_out*d_in)
+ *
+ * in place, float32. z_e is a standard normal from Philox4x32-10 (Salmon et
+ * al., SC'11) and Box-Muller (1958): key = (seed mod 2^32, seed >> 32);
+ * block j = e/4 has counter (j mod 2^32, j >> 32, layer->tensor_id, step);
+ * from its words (r0,r1,r2,r3): u = ((r>>8)+1) 2^-24 for r0, r2 and
+ * v = (r>>8) 2^-24 for r1, r3; z_{4j+0,1} = sqrt(-2 ln u_a)(cos, sin)(2 pi v_a),
+ * z_{4j+2,3} likewise from (u_b, v_b). sigma == 0 gives exactly scale*grad.
+ * Reads only d_in, d_out and tensor_id of the layer descriptor.
+ * sigma >= 0, C > 0 and finite, scale finite.
+ * ------------------------------------------------------------------------- */
+int dpsgd_add_noise(const dpsgd_layer* layer, float* grad, float sigma, float C,
+                    uint64_t seed, uint32_t step, float scale, void* stream);
+
+int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* const* grads,
+                          float sigma, float C, uint64_t seed, uint32_t step, float scale,
+                          void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Inspection hooks for tests (same stream as dpsgd_add_noise).
+ *   dpsgd_philox_u32: out[4*b + w] = word w of block (first_block + b), b < n_blocks.
+ *   dpsgd_gaussian:   out[e] = z_e of the stream above for e < n.
+ * out is a device pointer.
+ * ------------------------------------------------------------------------- */
+int dpsgd_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
+                     uint32_t tensor_id, uint32_t step, void* stream);
+int dpsgd_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                   void* stream);
+
+/* Static text for a dpsgd_status value. */
+const char* dpsgd_status_string(int status);
+
+/* Library version, for the binding's load check. */
+int dpsgd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPSGD_H_ */

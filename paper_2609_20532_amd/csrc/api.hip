@@ -1,0 +1,225 @@
+// C ABI of the DP-SGD gradient-step library: argument checks and dispatch.
+// The operations and their conventions are specified in include/dpsgd.h.
+#include <math.h>
+
+#include <vector>
+
+#include "common.h"
+
+namespace dpsgd {
+namespace {
+
+constexpr int64_t kI32Max = 0x7FFFFFFF;
+
+bool valid_dtype(int32_t d) { return d == DPSGD_F32 || d == DPSGD_BF16; }
+bool valid_mode(int32_t m) {
+  return m == DPSGD_NORM_AUTO || m == DPSGD_NORM_GHOST || m == DPSGD_NORM_MATERIALIZE;
+}
+
+// Shape checks shared by every layer-taking entry point. `data` also requires
+// the A and G pointers.
+int check_layer(const dpsgd_layer* L, bool data) {
+  if (!L) return DPSGD_ERR_INVALID_ARG;
+  if (!valid_dtype(L->dtype)) return DPSGD_ERR_UNSUPPORTED;
+  if (L->B < 1 || L->T < 1 || L->d_in < 1 || L->d_out < 1) return DPSGD_ERR_INVALID_ARG;
+  if (L->B > kI32Max || L->T > kI32Max || L->d_in > kI32Max || L->d_out > kI32Max)
+    return DPSGD_ERR_INVALID_ARG;
+  // Row and element counts must stay far inside int64 (and rows inside int32).
+  const int64_t rows = L->B * L->T;
+  if (rows > kI32Max) return DPSGD_ERR_INVALID_ARG;
+  if (L->d_in > (INT64_C(1) << 40) / rows || L->d_out > (INT64_C(1) << 40) / rows)
+    return DPSGD_ERR_INVALID_ARG;
+  if (L->d_out > (INT64_C(1) << 40) / L->d_in) return DPSGD_ERR_INVALID_ARG;
+  if (data && (!L->A || !L->G)) return DPSGD_ERR_INVALID_ARG;
+  return DPSGD_OK;
+}
+
+// Checks a layer array: every layer valid, one B and one dtype.
+int check_layers(const dpsgd_layer* layers, int32_t n, bool data) {
+  if (!layers || n < 1) return DPSGD_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n; ++l) {
+    const int st = check_layer(&layers[l], data);
+    if (st != DPSGD_OK) return st;
+    if (layers[l].B != layers[0].B) return DPSGD_ERR_INVALID_ARG;
+    if (layers[l].dtype != layers[0].dtype) return DPSGD_ERR_UNSUPPORTED;
+  }
+  return DPSGD_OK;
+}
+
+struct NormPlan {
+  std::vector<NormForm> forms;
+  std::vector<int64_t> cols;
+  int64_t P = 0;
+  size_t bytes = 0;
+};
+
+NormPlan plan_norms(const dpsgd_layer* layers, int32_t n, int32_t mode) {
+  NormPlan p;
+  p.forms.resize(n);
+  p.cols.resize(n);
+  for (int32_t l = 0; l < n; ++l) {
+    p.forms[l] = resolve_norm_form(layers[l], mode);
+    p.cols[l] = p.P;
+    p.P += norm_partials_per_example(layers[l], p.forms[l]);
+  }
+  p.bytes = round_up((size_t)layers[0].B * (size_t)p.P * sizeof(float), 256);
+  return p;
+}
+
+constexpr size_t kFactorBytesAlign = 256;
+
+size_t clip_ws_bytes(const dpsgd_layer* layers, int32_t n) {
+  size_t part = 0;
+  for (int32_t base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    ClipPlan plan;
+    plan_clip(layers + base, m, &plan);
+    if (plan.partial_bytes > part) part = plan.partial_bytes;
+  }
+  return round_up((size_t)layers[0].B * sizeof(float), kFactorBytesAlign) + part;
+}
+
+bool bad_float(float x) { return isnan(x); }
+
+}  // namespace
+}  // namespace dpsgd
+
+using namespace dpsgd;
+
+extern "C" {
+
+const char* dpsgd_status_string(int status) {
+  switch (status) {
+    case DPSGD_OK: return "ok";
+    case DPSGD_ERR_INVALID_ARG: return "invalid argument";
+    case DPSGD_ERR_UNSUPPORTED: return "unsupported dtype or mode";
+    case DPSGD_ERR_WORKSPACE: return "workspace missing or too small";
+    case DPSGD_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int dpsgd_version(void) { return 1; }
+
+size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode) {
+  if (check_layers(layers, n_layers, false) != DPSGD_OK || !valid_mode(mode)) return 0;
+  return plan_norms(layers, n_layers, mode).bytes;
+}
+
+int32_t dpsgd_select_norm_mode(const dpsgd_layer* layer) {
+  const int st = check_layer(layer, false);
+  if (st != DPSGD_OK) return st;
+  return resolve_norm_form(*layer, DPSGD_NORM_AUTO) == FORM_MAT ? DPSGD_NORM_MATERIALIZE
+                                                               : DPSGD_NORM_GHOST;
+}
+
+int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode,
+                                  float* norms_sq, int32_t accumulate, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  int st = check_layers(layers, n_layers, true);
+  if (st != DPSGD_OK) return st;
+  if (!valid_mode(mode)) return DPSGD_ERR_UNSUPPORTED;
+  if (!norms_sq) return DPSGD_ERR_INVALID_ARG;
+  const NormPlan p = plan_norms(layers, n_layers, mode);
+  if (!workspace || workspace_bytes < p.bytes) return DPSGD_ERR_WORKSPACE;
+  return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
+                      static_cast<float*>(workspace), p.P, p.cols.data(),
+                      static_cast<hipStream_t>(stream));
+}
+
+int dpsgd_per_example_norms(const dpsgd_layer* layer, int32_t mode, float* norms_sq,
+                            int32_t accumulate, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  return dpsgd_per_example_norms_multi(layer, 1, mode, norms_sq, accumulate, workspace,
+                                       workspace_bytes, stream);
+}
+
+int dpsgd_clip_factors(const float* norms_sq, int64_t B, float C, float* factors, uint8_t* mask,
+                       void* stream) {
+  if (!norms_sq || B < 1 || B > kI32Max) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(C) || !(C > 0.0f)) return DPSGD_ERR_INVALID_ARG;
+  return launch_clip_factors(norms_sq, B, C, nullptr, factors, mask,
+                             static_cast<hipStream_t>(stream));
+}
+
+size_t dpsgd_clip_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers) {
+  if (check_layers(layers, n_layers, false) != DPSGD_OK) return 0;
+  return clip_ws_bytes(layers, n_layers);
+}
+
+int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
+                                const float* norms_sq, float C, float* const* grads,
+                                int32_t accumulate, float* factors_out, uint8_t* mask_out,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_layers(layers, n_layers, true);
+  if (st != DPSGD_OK) return st;
+  if (!norms_sq || !grads) return DPSGD_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l)
+    if (!grads[l]) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(C) || !(C > 0.0f)) return DPSGD_ERR_INVALID_ARG;
+  const size_t need = clip_ws_bytes(layers, n_layers);
+  if (!workspace || workspace_bytes < need) return DPSGD_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t B = layers[0].B;
+  float* factors = static_cast<float*>(workspace);
+  float* partial_base = reinterpret_cast<float*>(
+      static_cast<char*>(workspace) + round_up((size_t)B * sizeof(float), kFactorBytesAlign));
+  st = launch_clip_factors(norms_sq, B, C, factors, factors_out, mask_out, s);
+  if (st != DPSGD_OK) return st;
+  for (int32_t base = 0; base < n_layers; base += kMaxLayersPerLaunch) {
+    const int m = n_layers - base < kMaxLayersPerLaunch ? n_layers - base : kMaxLayersPerLaunch;
+    ClipPlan plan;
+    plan_clip(layers + base, m, &plan);
+    st = launch_clip_sum(layers + base, m, factors, grads + base, accumulate ? 1 : 0,
+                         partial_base, plan, s);
+    if (st != DPSGD_OK) return st;
+  }
+  return DPSGD_OK;
+}
+
+int dpsgd_clip_accumulate(const dpsgd_layer* layer, const float* norms_sq, float C, float* grad,
+                          int32_t accumulate, float* factors_out, uint8_t* mask_out,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  float* grads[1] = {grad};
+  return dpsgd_clip_accumulate_multi(layer, 1, norms_sq, C, grads, accumulate, factors_out,
+                                     mask_out, workspace, workspace_bytes, stream);
+}
+
+int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* const* grads,
+                          float sigma, float C, uint64_t seed, uint32_t step, float scale,
+                          void* stream) {
+  int st = check_layers(layers, n_layers, false);
+  if (st != DPSGD_OK) return st;
+  if (!grads) return DPSGD_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l)
+    if (!grads[l]) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(sigma) || sigma < 0.0f || isinf(sigma)) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(C) || !(C > 0.0f) || isinf(C)) return DPSGD_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return DPSGD_ERR_INVALID_ARG;
+  return launch_noise(layers, n_layers, grads, sigma, C, seed, step, scale,
+                      static_cast<hipStream_t>(stream));
+}
+
+int dpsgd_add_noise(const dpsgd_layer* layer, float* grad, float sigma, float C, uint64_t seed,
+                    uint32_t step, float scale, void* stream) {
+  float* grads[1] = {grad};
+  return dpsgd_add_noise_multi(layer, 1, grads, sigma, C, seed, step, scale, stream);
+}
+
+int dpsgd_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
+                     uint32_t tensor_id, uint32_t step, void* stream) {
+  if (!out || first_block < 0 || n_blocks < 0) return DPSGD_ERR_INVALID_ARG;
+  if (n_blocks > (INT64_C(1) << 36)) return DPSGD_ERR_INVALID_ARG;
+  if (n_blocks == 0) return DPSGD_OK;
+  return launch_philox_u32(out, first_block, n_blocks, seed, tensor_id, step,
+                           static_cast<hipStream_t>(stream));
+}
+
+int dpsgd_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                   void* stream) {
+  if (!out || n < 0 || n > (INT64_C(1) << 38)) return DPSGD_ERR_INVALID_ARG;
+  if (n == 0) return DPSGD_OK;
+  return launch_gaussian(out, n, seed, tensor_id, step, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// Internal declarations shared by the library's HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dpsgd.h"
+
+namespace dpsgd {
+
+// ----------------------------------------------------------------- constants
+
+constexpr int kThreads = 256;          // every kernel uses 4 wave64s per workgroup
+constexpr int kMaxLayersPerLaunch = 48;  // entries of a per-launch layer table (kernarg space)
+
+// Norm form actually run for a layer (T = 1 always uses the closed form).
+enum NormForm : int { FORM_T1 = 0, FORM_GHOST = 1, FORM_MAT = 2 };
+
+// ----------------------------------------------------------- device helpers
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Round two floats to bf16 (nearest-even) and pack them (lo in bits 0..15).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  __bf16 a = (__bf16)lo;
+  __bf16 b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Deterministic sum over a wave64 (fixed butterfly order).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Deterministic sum over a 256-thread workgroup; result valid in every thread.
+// `red` is __shared__ float[4]. Contains barriers: call from uniform control flow.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wave] = v;
+  __syncthreads();
+  float r = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return r;
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ------------------------------------------------------------ host helpers
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// ------------------------------------------------------------ launchers
+// Each launcher validates nothing (the C ABI layer does) and returns a
+// dpsgd_status. Tables are built on the host and passed as kernel arguments.
+
+// Norm partial slots of one layer: how many float partials per example the
+// chosen form writes.
+int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form);
+NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode);
+
+// Writes per-example partials partials[i * P + col_l + j] for the given layers
+// (all with the chosen forms), then reduces them into norms_sq.
+int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
+                 float* norms_sq, int accumulate, float* partials, int64_t P,
+                 const int64_t* cols, hipStream_t stream);
+
+// Materialised-norm partials (gemm.hip) for the layers idx[0..n).
+int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                     float* partials, int64_t P, hipStream_t stream);
+
+int launch_clip_factors(const float* norms_sq, int64_t B, float C, float* factors,
+                        float* factors_out, uint8_t* mask_out, hipStream_t stream);
+
+// Split plan of the clip-weighted sum.
+struct ClipPlan {
+  int splits[kMaxLayersPerLaunch];
+  size_t partial_offset[kMaxLayersPerLaunch];  // bytes from the partial base
+  size_t partial_bytes;                          // total
+};
+void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan);
+
+int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factors,
+                    float* const* grads, int accumulate, float* partial_base,
+                    const ClipPlan& plan, hipStream_t stream);
+
+int launch_noise(const dpsgd_layer* layers, int n_layers, float* const* grads, float sigma,
+                 float C, uint64_t seed, uint32_t step, float scale, hipStream_t stream);
+
+int launch_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
+                      uint32_t tensor_id, uint32_t step, hipStream_t stream);
+int launch_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                    hipStream_t stream);
+
+inline int check_launch() {
+  return hipGetLastError() == hipSuccess ? DPSGD_OK : DPSGD_ERR_HIP;
+}
+
+}  // namespace dpsgd

@@ -1,0 +1,195 @@
+// Gaussian noise of the DP-SGD step: Philox4x32-10 + Box-Muller, added in place.
+//
+// Paper: Section 2.2, z_t ~ N(0, sigma^2 C^2 I) added to the clipped sum and
+// scaled by 1/|B_t|; GPU-side algorithm, noise step. The generator is
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) with the Box-Muller (1958)
+// transform; the paper does not fix one.
+//
+// The pass is bound by HBM traffic (read + write of 4 bytes per element) and,
+// close behind, by integer/transcendental ALU work: one Philox block (ten
+// rounds, two 32x32->64 products each) and two log/sqrt/sin/cos sets per four
+// elements. Each thread owns whole 16-byte blocks so loads and stores are
+// 16-byte, fully coalesced, and every launch covers all tensors of the call.
+#include "common.h"
+
+namespace dpsgd {
+namespace {
+
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kWeyl0 = 0x9E3779B9u;
+constexpr uint32_t kWeyl1 = 0xBB67AE85u;
+
+__device__ __forceinline__ uint4 philox4x32_10(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
+                                               uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)x0 * kPhiloxM0;
+    const uint64_t p1 = (uint64_t)x2 * kPhiloxM1;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    x1 = (uint32_t)p1;
+    x3 = (uint32_t)p0;
+    x0 = n0;
+    x2 = n2;
+    k0 += kWeyl0;
+    k1 += kWeyl1;
+  }
+  return make_uint4(x0, x1, x2, x3);
+}
+
+// Four standard normals from one block: lanes (0,1) from (r0,r1), (2,3) from (r2,r3).
+// u in (0,1] and v in [0,1) are exact; sin/cos take their argument in turns.
+__device__ __forceinline__ float4 box_muller4(uint4 r) {
+  const float ua = (float)((r.x >> 8) + 1u) * 0x1p-24f;
+  const float va = (float)(r.y >> 8) * 0x1p-24f;
+  const float ub = (float)((r.z >> 8) + 1u) * 0x1p-24f;
+  const float vb = (float)(r.w >> 8) * 0x1p-24f;
+  const float ra = sqrtf(-2.0f * logf(ua));
+  const float rb = sqrtf(-2.0f * logf(ub));
+  return make_float4(ra * __builtin_amdgcn_cosf(va), ra * __builtin_amdgcn_sinf(va),
+                     rb * __builtin_amdgcn_cosf(vb), rb * __builtin_amdgcn_sinf(vb));
+}
+
+__device__ __forceinline__ float4 normals_of_block(uint64_t j, uint32_t tensor_id, uint32_t step,
+                                                    uint32_t k0, uint32_t k1) {
+  return box_muller4(philox4x32_10((uint32_t)j, (uint32_t)(j >> 32), tensor_id, step, k0, k1));
+}
+
+struct NoiseSeg {
+  float* ptr;
+  int64_t numel;
+  uint32_t tensor_id;
+  uint32_t wg_begin;   // first workgroup of this tensor in the launch
+  uint32_t aligned;    // ptr is 16-byte aligned
+  uint32_t pad;
+};
+
+struct NoiseArgs {
+  NoiseSeg seg[kMaxLayersPerLaunch];
+  int n_seg;
+  uint32_t k0, k1, step;
+  float sigmaC, scale;
+};
+
+constexpr int kBlocksPerThread = 4;
+constexpr int kBlocksPerWG = kThreads * kBlocksPerThread;
+
+__global__ __launch_bounds__(kThreads) void noise_kernel(NoiseArgs args) {
+  // Segment of this workgroup: binary search over wg_begin (uniform).
+  int lo = 0, hi = args.n_seg - 1;
+  const uint32_t wg = blockIdx.x;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.seg[mid].wg_begin <= wg) lo = mid; else hi = mid - 1;
+  }
+  const NoiseSeg s = args.seg[lo];
+  const int64_t first_block = (int64_t)(wg - s.wg_begin) * kBlocksPerWG;
+  const int64_t n_blocks = (s.numel + 3) >> 2;
+  const float sc = args.scale, sgc = args.sigmaC;
+  const bool with_noise = sgc != 0.0f;
+
+#pragma unroll
+  for (int u = 0; u < kBlocksPerThread; ++u) {
+    const int64_t j = first_block + (int64_t)u * kThreads + threadIdx.x;
+    if (j >= n_blocks) break;
+    float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (with_noise) z = normals_of_block((uint64_t)j, s.tensor_id, args.step, args.k0, args.k1);
+    const int64_t e0 = j * 4;
+    if (s.aligned && e0 + 4 <= s.numel) {
+      float4* p = reinterpret_cast<float4*>(s.ptr + e0);
+      float4 g = *p;
+      g.x = sc * fmaf(sgc, z.x, g.x);
+      g.y = sc * fmaf(sgc, z.y, g.y);
+      g.z = sc * fmaf(sgc, z.z, g.z);
+      g.w = sc * fmaf(sgc, z.w, g.w);
+      *p = g;
+    } else {
+      const float zz[4] = {z.x, z.y, z.z, z.w};
+      for (int w = 0; w < 4; ++w) {
+        if (e0 + w < s.numel) {
+          float* p = s.ptr + e0 + w;
+          *p = sc * fmaf(sgc, zz[w], *p);
+        }
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void philox_u32_kernel(uint32_t* out, int64_t first_block,
+                                                              int64_t n_blocks, uint32_t k0,
+                                                              uint32_t k1, uint32_t tensor_id,
+                                                              uint32_t step) {
+  const int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (b >= n_blocks) return;
+  const uint64_t j = (uint64_t)(first_block + b);
+  const uint4 w = philox4x32_10((uint32_t)j, (uint32_t)(j >> 32), tensor_id, step, k0, k1);
+  out[4 * b + 0] = w.x;
+  out[4 * b + 1] = w.y;
+  out[4 * b + 2] = w.z;
+  out[4 * b + 3] = w.w;
+}
+
+__global__ __launch_bounds__(kThreads) void gaussian_kernel(float* out, int64_t n, uint32_t k0,
+                                                            uint32_t k1, uint32_t tensor_id,
+                                                            uint32_t step) {
+  const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t e0 = j * 4;
+  if (e0 >= n) return;
+  const float4 z = normals_of_block((uint64_t)j, tensor_id, step, k0, k1);
+  const float zz[4] = {z.x, z.y, z.z, z.w};
+  for (int w = 0; w < 4; ++w)
+    if (e0 + w < n) out[e0 + w] = zz[w];
+}
+
+}  // namespace
+
+int launch_noise(const dpsgd_layer* layers, int n_layers, float* const* grads, float sigma,
+                 float C, uint64_t seed, uint32_t step, float scale, hipStream_t stream) {
+  for (int base = 0; base < n_layers; base += kMaxLayersPerLaunch) {
+    const int n = n_layers - base < kMaxLayersPerLaunch ? n_layers - base : kMaxLayersPerLaunch;
+    NoiseArgs args{};
+    args.n_seg = n;
+    args.k0 = (uint32_t)seed;
+    args.k1 = (uint32_t)(seed >> 32);
+    args.step = step;
+    args.sigmaC = sigma * C;
+    args.scale = scale;
+    int64_t wgs = 0;
+    for (int l = 0; l < n; ++l) {
+      const dpsgd_layer& L = layers[base + l];
+      NoiseSeg& s = args.seg[l];
+      s.ptr = grads[base + l];
+      s.numel = L.d_out * L.d_in;
+      s.tensor_id = L.tensor_id;
+      s.wg_begin = (uint32_t)wgs;
+      s.aligned = aligned16(s.ptr) ? 1u : 0u;
+      wgs += ceil_div(ceil_div(s.numel, 4), kBlocksPerWG);
+    }
+    if (wgs <= 0) continue;
+    if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(noise_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, args);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
+}
+
+int launch_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
+                      uint32_t tensor_id, uint32_t step, hipStream_t stream) {
+  const int64_t wgs = ceil_div(n_blocks, kThreads);
+  if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(philox_u32_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, out,
+                     first_block, n_blocks, (uint32_t)seed, (uint32_t)(seed >> 32), tensor_id, step);
+  return check_launch();
+}
+
+int launch_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, uint32_t step,
+                    hipStream_t stream) {
+  const int64_t wgs = ceil_div(ceil_div(n, 4), kThreads);
+  if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(gaussian_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, out, n,
+                     (uint32_t)seed, (uint32_t)(seed >> 32), tensor_id, step);
+  return check_launch();
+}
+
+}  // namespace dpsgd

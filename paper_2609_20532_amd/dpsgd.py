@@ -1,0 +1,304 @@
+"""Python binding of the C ABI in ``include/dpsgd.h`` (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of the DP-SGD step: it converts torch tensors to device pointers,
+fills ``dpsgd_layer`` descriptors, passes torch's current HIP stream, and
+raises :class:`DpsgdError` on a non-zero status. torch supplies device memory
+and streams only. The library must be built (``paper_2609_20532_amd.build``);
+loading fails loudly when it is missing.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libdpsgd.so")
+
+DPSGD_F32 = 0
+DPSGD_BF16 = 1
+DPSGD_NORM_AUTO = 0
+DPSGD_NORM_GHOST = 1
+DPSGD_NORM_MATERIALIZE = 2
+
+DPSGD_OK = 0
+DPSGD_ERR_INVALID_ARG = -1
+DPSGD_ERR_UNSUPPORTED = -2
+DPSGD_ERR_WORKSPACE = -3
+DPSGD_ERR_HIP = -4
+
+#: Every symbol the header declares (checked by the CPU test suite).
+EXPORTED = (
+    "dpsgd_norms_workspace_bytes", "dpsgd_select_norm_mode", "dpsgd_per_example_norms",
+    "dpsgd_per_example_norms_multi", "dpsgd_clip_factors", "dpsgd_clip_workspace_bytes",
+    "dpsgd_clip_accumulate", "dpsgd_clip_accumulate_multi", "dpsgd_add_noise",
+    "dpsgd_add_noise_multi", "dpsgd_philox_u32", "dpsgd_gaussian", "dpsgd_status_string",
+    "dpsgd_version",
+)
+
+
+class DpsgdError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__(f"{fn} failed: {text} (status {status})")
+        self.status = status
+
+
+class dpsgd_layer(ctypes.Structure):  # noqa: N801 - mirrors the C struct name
+    _fields_ = [
+        ("A", ctypes.c_void_p),
+        ("G", ctypes.c_void_p),
+        ("B", ctypes.c_int64),
+        ("T", ctypes.c_int64),
+        ("d_in", ctypes.c_int64),
+        ("d_out", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+        ("tensor_id", ctypes.c_uint32),
+    ]
+
+
+_lib = None
+
+
+def _declare(lib):
+    P = ctypes.POINTER
+    L = P(dpsgd_layer)
+    vp, i32, i64, u32, u64, f32, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                       ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float,
+                                       ctypes.c_size_t)
+    sig = {
+        "dpsgd_norms_workspace_bytes": (sz, [L, i32, i32]),
+        "dpsgd_select_norm_mode": (i32, [L]),
+        "dpsgd_per_example_norms": (ctypes.c_int, [L, i32, vp, i32, vp, sz, vp]),
+        "dpsgd_per_example_norms_multi": (ctypes.c_int, [L, i32, i32, vp, i32, vp, sz, vp]),
+        "dpsgd_clip_factors": (ctypes.c_int, [vp, i64, f32, vp, vp, vp]),
+        "dpsgd_clip_workspace_bytes": (sz, [L, i32]),
+        "dpsgd_clip_accumulate": (ctypes.c_int, [L, vp, f32, vp, i32, vp, vp, vp, sz, vp]),
+        "dpsgd_clip_accumulate_multi": (ctypes.c_int,
+                                        [L, i32, vp, f32, P(vp), i32, vp, vp, vp, sz, vp]),
+        "dpsgd_add_noise": (ctypes.c_int, [L, vp, f32, f32, u64, u32, f32, vp]),
+        "dpsgd_add_noise_multi": (ctypes.c_int, [L, i32, P(vp), f32, f32, u64, u32, f32, vp]),
+        "dpsgd_philox_u32": (ctypes.c_int, [vp, i64, i64, u64, u32, u32, vp]),
+        "dpsgd_gaussian": (ctypes.c_int, [vp, i64, u64, u32, u32, vp]),
+        "dpsgd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "dpsgd_version": (ctypes.c_int, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+
+
+def load(path: str | None = None):
+    """Load ``libdpsgd.so`` (after torch, so both share one HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (loads the HIP runtime the library links against)
+
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_20532_amd.build`")
+    lib = ctypes.CDLL(path)
+    _declare(lib)
+    if lib.dpsgd_version() != 1:
+        raise RuntimeError("libdpsgd version mismatch")
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, status: int):
+    if status != DPSGD_OK:
+        raise DpsgdError(fn, status, _lib.dpsgd_status_string(status).decode())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+# ----------------------------------------------------------------- descriptors
+
+
+def make_layer(A, G, tensor_id: int = 0) -> dpsgd_layer:
+    """Descriptor of one layer from device tensors A [B,T,d_in] and G [B,T,d_out]."""
+    import torch
+    if A.dim() != 3 or G.dim() != 3 or A.shape[:2] != G.shape[:2]:
+        raise ValueError("A must be [B,T,d_in] and G [B,T,d_out] with the same B, T")
+    if A.dtype != G.dtype or A.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("A and G must both be float32 or both bfloat16")
+    if not (A.is_contiguous() and G.is_contiguous()):
+        raise ValueError("A and G must be contiguous")
+    if not (A.is_cuda and G.is_cuda):
+        raise ValueError("A and G must be device tensors")
+    B, T, d_in = A.shape
+    return dpsgd_layer(A.data_ptr(), G.data_ptr(), B, T, d_in, G.shape[2],
+                       DPSGD_BF16 if A.dtype == torch.bfloat16 else DPSGD_F32, tensor_id)
+
+
+def shape_layer(B: int, T: int, d_in: int, d_out: int, dtype: int = DPSGD_BF16,
+                tensor_id: int = 0) -> dpsgd_layer:
+    """Descriptor with no data, for workspace queries and noise calls."""
+    return dpsgd_layer(None, None, B, T, d_in, d_out, dtype, tensor_id)
+
+
+def _array(layers):
+    if isinstance(layers, dpsgd_layer):
+        layers = [layers]
+    arr = (dpsgd_layer * len(layers))(*layers)
+    return arr, len(layers)
+
+
+def _ptr_array(tensors):
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+# ------------------------------------------------------------- entry points
+
+
+def dpsgd_norms_workspace_bytes(layers, mode: int = DPSGD_NORM_AUTO) -> int:
+    load()
+    arr, n = _array(layers)
+    return int(_lib.dpsgd_norms_workspace_bytes(arr, n, mode))
+
+
+def dpsgd_select_norm_mode(layer: dpsgd_layer) -> int:
+    load()
+    r = int(_lib.dpsgd_select_norm_mode(ctypes.byref(layer)))
+    if r < 0:
+        _check("dpsgd_select_norm_mode", r)
+    return r
+
+
+def dpsgd_per_example_norms(layer, mode, norms_sq, accumulate=False, workspace=None,
+                            stream=None):
+    load()
+    st = _lib.dpsgd_per_example_norms(ctypes.byref(layer), mode, _ptr(norms_sq), int(accumulate),
+                                      _ptr(workspace),
+                                      0 if workspace is None else workspace.numel(),
+                                      _stream(stream))
+    _check("dpsgd_per_example_norms", st)
+
+
+def dpsgd_per_example_norms_multi(layers, mode, norms_sq, accumulate=False, workspace=None,
+                                  stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_per_example_norms_multi(arr, n, mode, _ptr(norms_sq), int(accumulate),
+                                            _ptr(workspace),
+                                            0 if workspace is None else workspace.numel(),
+                                            _stream(stream))
+    _check("dpsgd_per_example_norms_multi", st)
+
+
+def dpsgd_clip_factors(norms_sq, C: float, factors=None, mask=None, stream=None):
+    load()
+    st = _lib.dpsgd_clip_factors(_ptr(norms_sq), norms_sq.numel(), C, _ptr(factors), _ptr(mask),
+                                 _stream(stream))
+    _check("dpsgd_clip_factors", st)
+
+
+def dpsgd_clip_workspace_bytes(layers) -> int:
+    load()
+    arr, n = _array(layers)
+    return int(_lib.dpsgd_clip_workspace_bytes(arr, n))
+
+
+def dpsgd_clip_accumulate(layer, norms_sq, C, grad, accumulate=False, factors_out=None,
+                          mask_out=None, workspace=None, stream=None):
+    load()
+    st = _lib.dpsgd_clip_accumulate(ctypes.byref(layer), _ptr(norms_sq), C, _ptr(grad),
+                                    int(accumulate), _ptr(factors_out), _ptr(mask_out),
+                                    _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                    _stream(stream))
+    _check("dpsgd_clip_accumulate", st)
+
+
+def dpsgd_clip_accumulate_multi(layers, norms_sq, C, grads, accumulate=False, factors_out=None,
+                                mask_out=None, workspace=None, stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_clip_accumulate_multi(arr, n, _ptr(norms_sq), C, _ptr_array(grads),
+                                          int(accumulate), _ptr(factors_out), _ptr(mask_out),
+                                          _ptr(workspace),
+                                          0 if workspace is None else workspace.numel(),
+                                          _stream(stream))
+    _check("dpsgd_clip_accumulate_multi", st)
+
+
+def dpsgd_add_noise(layer, grad, sigma, C, seed, step, scale, stream=None):
+    load()
+    st = _lib.dpsgd_add_noise(ctypes.byref(layer), _ptr(grad), sigma, C, seed, step, scale,
+                              _stream(stream))
+    _check("dpsgd_add_noise", st)
+
+
+def dpsgd_add_noise_multi(layers, grads, sigma, C, seed, step, scale, stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_add_noise_multi(arr, n, _ptr_array(grads), sigma, C, seed, step, scale,
+                                    _stream(stream))
+    _check("dpsgd_add_noise_multi", st)
+
+
+def dpsgd_philox_u32(out, first_block, n_blocks, seed, tensor_id, step, stream=None):
+    load()
+    st = _lib.dpsgd_philox_u32(_ptr(out), first_block, n_blocks, seed, tensor_id, step,
+                               _stream(stream))
+    _check("dpsgd_philox_u32", st)
+
+
+def dpsgd_gaussian(out, n, seed, tensor_id, step, stream=None):
+    load()
+    st = _lib.dpsgd_gaussian(_ptr(out), n, seed, tensor_id, step, _stream(stream))
+    _check("dpsgd_gaussian", st)
+
+
+# ------------------------------------------------------------ whole step
+
+
+@dataclass
+class StepBuffers:
+    """Device buffers of one step: norms, factors, mask, workspaces, grads."""
+
+    norms_sq: object
+    factors: object
+    mask: object
+    norms_ws: object
+    clip_ws: object
+    grads: list
+
+
+def alloc_step(layers, mode: int = DPSGD_NORM_AUTO, device="cuda") -> StepBuffers:
+    """Allocate (with torch) every buffer a step over ``layers`` needs."""
+    import torch
+    B = layers[0].B
+    nb = dpsgd_norms_workspace_bytes(layers, mode)
+    cb = dpsgd_clip_workspace_bytes(layers)
+    return StepBuffers(
+        norms_sq=torch.empty(B, dtype=torch.float32, device=device),
+        factors=torch.empty(B, dtype=torch.float32, device=device),
+        mask=torch.empty(B, dtype=torch.uint8, device=device),
+        norms_ws=torch.empty(max(nb, 1), dtype=torch.uint8, device=device),
+        clip_ws=torch.empty(max(cb, 1), dtype=torch.uint8, device=device),
+        grads=[torch.empty((L.d_out, L.d_in), dtype=torch.float32, device=device)
+               for L in layers],
+    )
+
+
+def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
+             scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, stream=None):
+    """One DP-SGD gradient step: global norms, clip + sum, noise (three ABI calls)."""
+    dpsgd_per_example_norms_multi(layers, mode, buf.norms_sq, accumulate=False,
+                                  workspace=buf.norms_ws, stream=stream)
+    dpsgd_clip_accumulate_multi(layers, buf.norms_sq, C, buf.grads, accumulate=False,
+                                factors_out=buf.factors, mask_out=buf.mask,
+                                workspace=buf.clip_ws, stream=stream)
+    dpsgd_add_noise_multi(layers, buf.grads, sigma, C, seed, step, scale, stream=stream)

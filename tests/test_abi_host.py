@@ -1,0 +1,139 @@
+"""Host-side checks of the C ABI library (CPU only: no kernel is launched).
+
+The library loads, exports every function ``include/dpsgd.h`` declares, and
+rejects bad arguments before enqueuing anything.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_20532_amd import dpsgd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return dpsgd.load()
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "dpsgd.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dpsgd_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(lib):
+    names = _declared_functions()
+    assert len(names) >= 14
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(dpsgd.EXPORTED)
+
+
+def test_status_strings(lib):
+    for st in (0, -1, -2, -3, -4, 99):
+        assert isinstance(lib.dpsgd_status_string(st), bytes)
+    assert lib.dpsgd_status_string(-3) == b"workspace missing or too small"
+
+
+def test_layer_struct_layout():
+    assert ctypes.sizeof(dpsgd.dpsgd_layer) == 56
+    assert dpsgd.dpsgd_layer.dtype.offset == 48
+
+
+def test_workspace_queries_and_mode_selection(lib):
+    c3 = dpsgd.shape_layer(64, 512, 768, 3072)
+    assert dpsgd.dpsgd_select_norm_mode(c3) == dpsgd.DPSGD_NORM_GHOST
+    lora = dpsgd.shape_layer(16, 1024, 4096, 16)
+    assert dpsgd.dpsgd_select_norm_mode(lora) == dpsgd.DPSGD_NORM_MATERIALIZE
+    # 4 T-tiles -> 10 upper-triangle tile pairs per example
+    assert dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 64 * 10 * 4 + 0 \
+        or dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 2560
+    t1 = dpsgd.shape_layer(32, 1, 256, 128, dpsgd.DPSGD_F32)
+    assert dpsgd.dpsgd_norms_workspace_bytes(t1) == 256   # one partial per example, rounded
+    assert dpsgd.dpsgd_clip_workspace_bytes(t1) > 0
+    bad = dpsgd.shape_layer(0, 1, 4, 4)
+    assert dpsgd.dpsgd_norms_workspace_bytes(bad) == 0
+    with pytest.raises(dpsgd.DpsgdError):
+        dpsgd.dpsgd_select_norm_mode(bad)
+
+
+def _lay(**kw):
+    base = dict(A=16, G=32, B=2, T=3, d_in=4, d_out=5, dtype=1, tensor_id=0)
+    base.update(kw)
+    return dpsgd.dpsgd_layer(base["A"], base["G"], base["B"], base["T"], base["d_in"],
+                             base["d_out"], base["dtype"], base["tensor_id"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), -1), (dict(T=0), -1), (dict(d_in=-3), -1), (dict(d_out=0), -1),
+    (dict(A=None), -1), (dict(G=None), -1), (dict(dtype=7), -2),
+    (dict(B=1 << 40), -1), (dict(d_in=1 << 31, d_out=1 << 31), -1),
+])
+def test_norms_rejects_bad_layers(lib, kw, status):
+    L = _lay(**kw)
+    st = lib.dpsgd_per_example_norms(ctypes.byref(L), 0, ctypes.c_void_p(64), 0,
+                                     ctypes.c_void_p(128), 1 << 20, None)
+    assert st == status
+
+
+def test_norms_rejects_bad_mode_and_workspace(lib):
+    L = _lay()
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), 5, ctypes.c_void_p(64), 0,
+                                       ctypes.c_void_p(128), 1 << 20, None) == -2
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), 0, None, 0,
+                                       ctypes.c_void_p(128), 1 << 20, None) == -1
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), 0, ctypes.c_void_p(64), 0,
+                                       ctypes.c_void_p(128), 0, None) == -3
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), 0, ctypes.c_void_p(64), 0,
+                                       None, 1 << 20, None) == -3
+
+
+def test_multi_rejects_mixed_batches_and_dtypes(lib):
+    arr = (dpsgd.dpsgd_layer * 2)(_lay(), _lay(B=3))
+    assert lib.dpsgd_per_example_norms_multi(arr, 2, 0, ctypes.c_void_p(64), 0,
+                                             ctypes.c_void_p(128), 1 << 20, None) == -1
+    arr = (dpsgd.dpsgd_layer * 2)(_lay(), _lay(dtype=0))
+    assert lib.dpsgd_per_example_norms_multi(arr, 2, 0, ctypes.c_void_p(64), 0,
+                                             ctypes.c_void_p(128), 1 << 20, None) == -2
+    assert lib.dpsgd_per_example_norms_multi(arr, 0, 0, ctypes.c_void_p(64), 0,
+                                             ctypes.c_void_p(128), 1 << 20, None) == -1
+
+
+@pytest.mark.parametrize("C", [0.0, -1.0, float("nan")])
+def test_clip_rejects_bad_C(lib, C):
+    L = _lay()
+    st = lib.dpsgd_clip_accumulate(ctypes.byref(L), ctypes.c_void_p(64), C, ctypes.c_void_p(256),
+                                   0, None, None, ctypes.c_void_p(512), 1 << 20, None)
+    assert st == -1
+    assert lib.dpsgd_clip_factors(ctypes.c_void_p(64), 4, C, None, None, None) == -1
+
+
+def test_clip_rejects_null_grad_and_small_workspace(lib):
+    L = _lay()
+    assert lib.dpsgd_clip_accumulate(ctypes.byref(L), ctypes.c_void_p(64), 1.0, None, 0, None,
+                                     None, ctypes.c_void_p(512), 1 << 20, None) == -1
+    assert lib.dpsgd_clip_accumulate(ctypes.byref(L), ctypes.c_void_p(64), 1.0,
+                                     ctypes.c_void_p(256), 0, None, None, ctypes.c_void_p(512),
+                                     8, None) == -3
+
+
+@pytest.mark.parametrize("sigma,C,scale", [(-1.0, 1.0, 1.0), (float("nan"), 1.0, 1.0),
+                                           (1.0, 0.0, 1.0), (1.0, float("inf"), 1.0),
+                                           (1.0, 1.0, float("inf")), (float("inf"), 1.0, 1.0)])
+def test_noise_rejects_bad_scalars(lib, sigma, C, scale):
+    L = _lay()
+    assert lib.dpsgd_add_noise(ctypes.byref(L), ctypes.c_void_p(256), sigma, C, 1, 0, scale,
+                               None) == -1
+
+
+def test_hooks_reject_bad_args_and_accept_empty(lib):
+    assert lib.dpsgd_philox_u32(None, 0, 4, 1, 0, 0, None) == -1
+    assert lib.dpsgd_philox_u32(ctypes.c_void_p(64), -1, 4, 1, 0, 0, None) == -1
+    assert lib.dpsgd_philox_u32(ctypes.c_void_p(64), 0, 0, 1, 0, 0, None) == 0
+    assert lib.dpsgd_gaussian(ctypes.c_void_p(64), -5, 1, 0, 0, None) == -1
+    assert lib.dpsgd_gaussian(ctypes.c_void_p(64), 0, 1, 0, 0, None) == 0

@@ -1,0 +1,350 @@
+"""GPU parity: the HIP library (through the C ABI) against the float64 oracle.
+
+Every test draws seeded inputs, runs the library on the GPU, runs the oracle on
+the same stored values, and compares element by element: bit-exact for the
+Philox words and the clip mask, relative tolerances for floating point (1e-4
+for float32 inputs, 2e-2 for bfloat16 inputs; tighter bounds derived from the
+arithmetic are asserted too where they apply).
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import philox
+from paper_2609_20532_amd import workloads as wl
+
+from parity_util import (TOL, assert_sum_close, device_layers, guard_band, oracle_layers,
+                         rel_err, to_device, torch_to_float64)
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    _log(f"[gpu] start {request.node.name}")
+    yield
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+# --------------------------------------------------------------- Philox / noise
+
+
+@pytest.mark.parametrize("seed,tensor_id,step,first,n", [
+    (42, 0, 0, 0, 4096),
+    (7, 47, 3, 123457, 1001),
+    (0xFFFFFFFFFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, (1 << 32) - 500, 1000),  # crosses 2^32 blocks
+])
+def test_philox_stream_bit_exact(dp, seed, tensor_id, step, first, n):
+    import torch
+    out = torch.empty(4 * n, dtype=torch.int32, device="cuda")
+    dp.dpsgd_philox_u32(out, first, n, seed, tensor_id, step)
+    _sync()
+    got = out.cpu().numpy().view(np.uint32).reshape(n, 4)
+    ref = philox.philox_blocks(n, seed, tensor_id, step, first_block=first)
+    np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 1023, 200_001])
+def test_gaussian_matches_oracle(dp, n):
+    import torch
+    out = torch.empty(n, dtype=torch.float32, device="cuda")
+    dp.dpsgd_gaussian(out, n, 42, 5, 2)
+    _sync()
+    got = out.cpu().numpy().astype(np.float64)
+    ref = philox.gaussian_stream(n, 42, 5, 2)
+    err = np.abs(got - ref) / (1.0 + np.abs(ref))
+    assert float(err.max()) <= 1e-5, f"max normalised error {err.max():.3e}"
+
+
+def _noise_case(dp, d_out, d_in, sigma, C, scale, seed, tensor_id, step, offset=0):
+    import torch
+    rng = np.random.default_rng(d_out * 1000 + d_in)
+    S = rng.standard_normal((d_out, d_in)).astype(np.float32)
+    buf = torch.zeros(d_out * d_in + offset, dtype=torch.float32, device="cuda")
+    view = buf[offset:offset + d_out * d_in]
+    view.copy_(torch.from_numpy(S.reshape(-1)))
+    L = dp.shape_layer(1, 1, d_in, d_out, dp.DPSGD_F32, tensor_id)
+    dp.dpsgd_add_noise(L, view, sigma, C, seed, step, scale)
+    _sync()
+    got = view.cpu().numpy().reshape(d_out, d_in)
+    return S, got
+
+
+@pytest.mark.parametrize("d_out,d_in,offset", [(128, 256, 0), (37, 19, 0), (10, 512, 1), (3, 1, 0)])
+def test_noise_sigma_zero_is_exact_scale(dp, d_out, d_in, offset):
+    S, got = _noise_case(dp, d_out, d_in, 0.0, 1.0, 1.0 / 64, 42, 0, 0, offset)
+    np.testing.assert_array_equal(got, (S * np.float32(1.0 / 64)).astype(np.float32))
+
+
+@pytest.mark.parametrize("d_out,d_in,offset,sigma,C,scale", [
+    (128, 256, 0, 1.0, 1.0, 1.0),
+    (37, 19, 0, 1.1, 1.0, 1.0 / 256),      # numel % 4 != 0
+    (10, 512, 1, 0.8, 0.5, 1.0),           # pointer not 16-byte aligned
+    (768, 768, 0, 1.0, 1.0, 1.0 / 128),
+])
+def test_noise_matches_oracle(dp, d_out, d_in, offset, sigma, C, scale):
+    S, got = _noise_case(dp, d_out, d_in, sigma, C, scale, 7, 3, 0, offset)
+    ref = oracle.add_noise(S.astype(np.float64), sigma, C, 7, 3, 0, scale)
+    # Each entry: float32 rounding of S + sigma*C*z plus the normal's own error.
+    err = np.abs(got - ref) / (np.abs(scale) * (1.0 + np.abs(S) + sigma * C * 6.0))
+    assert float(err.max()) <= 1e-5, f"max normalised error {err.max():.3e}"
+
+
+# ------------------------------------------------------------------ norms
+
+NORM_SHAPES = [
+    # B, T, d_in, d_out
+    (4, 1, 256, 128),
+    (3, 2, 24, 40),
+    (3, 17, 96, 200),      # T < tile, ragged d
+    (2, 130, 136, 72),     # two T tiles, ragged tail
+    (2, 300, 64, 264),     # three T tiles
+    (2, 64, 300, 10),      # d_out < 16
+    (2, 40, 13, 21),       # d not a multiple of the vector width
+]
+
+
+def _host_layer(B, T, d_in, d_out, dtype, seed, a_scale=1.0, g_scale=0.1, tensor_id=0):
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((B, T, d_in)) * a_scale
+    G = rng.standard_normal((B, T, d_out)) * g_scale
+    store = (lambda x: wl.bf16_bits_from_f32(x.astype(np.float32))) if dtype == wl.BF16 \
+        else (lambda x: x.astype(np.float32))
+    return wl.HostLayer(A=store(A), G=store(G), d_in=d_in, d_out=d_out, tensor_id=tensor_id,
+                        dtype=dtype)
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("mode", [1, 2])  # GHOST, MATERIALIZE
+@pytest.mark.parametrize("shape", NORM_SHAPES)
+def test_norms_match_oracle(dp, dtype, mode, shape):
+    import torch
+    B, T, d_in, d_out = shape
+    h = _host_layer(B, T, d_in, d_out, dtype, seed=sum(shape) + mode)
+    (L, A, G), = device_layers([h])
+    ws = torch.empty(max(dp.dpsgd_norms_workspace_bytes(L, mode), 1), dtype=torch.uint8,
+                     device="cuda")
+    nsq = torch.full((B,), 123.0, dtype=torch.float32, device="cuda")
+    dp.dpsgd_per_example_norms(L, mode, nsq, accumulate=False, workspace=ws)
+    _sync()
+    got = np.sqrt(torch_to_float64(nsq))
+    ref = np.sqrt(oracle.per_example_norms_sq(oracle_layers([h])))
+    err = np.abs(got - ref) / ref
+    _log(f"norm rel err max {err.max():.2e}")
+    assert float(err.max()) <= TOL[dtype]
+    # bf16 products are exact in fp32 and only the fp32 sums round.
+    assert float(err.max()) <= 1e-4
+
+
+def test_norms_accumulate_over_layers(dp):
+    """Per-layer calls with accumulate equal one multi-layer call (global norm)."""
+    import torch
+    hs = [_host_layer(3, 20, 40, 24, wl.BF16, seed=1, tensor_id=0),
+          _host_layer(3, 20, 24, 56, wl.BF16, seed=2, tensor_id=1),
+          _host_layer(3, 20, 56, 8, wl.BF16, seed=3, tensor_id=2)]
+    dl = device_layers(hs)
+    Ls = [x[0] for x in dl]
+    ws = torch.empty(dp.dpsgd_norms_workspace_bytes(Ls, 0), dtype=torch.uint8, device="cuda")
+    multi = torch.empty(3, dtype=torch.float32, device="cuda")
+    dp.dpsgd_per_example_norms_multi(Ls, 0, multi, workspace=ws)
+    seq = torch.empty(3, dtype=torch.float32, device="cuda")
+    for k, L in enumerate(Ls):
+        wsl = torch.empty(dp.dpsgd_norms_workspace_bytes(L, 0), dtype=torch.uint8, device="cuda")
+        dp.dpsgd_per_example_norms(L, 0, seq, accumulate=k > 0, workspace=wsl)
+    _sync()
+    ref = oracle.per_example_norms_sq(oracle_layers(hs))
+    assert rel_err(torch_to_float64(multi), ref) <= 1e-5
+    assert rel_err(torch_to_float64(seq), ref) <= 1e-5
+
+
+# ------------------------------------------------------------ clip factors
+
+
+def test_clip_factors_and_mask_exact(dp):
+    import torch
+    C = 1.0
+    rng = np.random.default_rng(5)
+    n = np.concatenate([rng.uniform(0.01, 0.99, 100), rng.uniform(1.01, 50, 100),
+                        [0.0, 1e-30, 1e30]])
+    nsq = (n * n).astype(np.float32)
+    t = torch.from_numpy(nsq).cuda()
+    f = torch.empty_like(t)
+    m = torch.empty(len(n), dtype=torch.uint8, device="cuda")
+    dp.dpsgd_clip_factors(t, C, f, m)
+    _sync()
+    n_ref, c_ref, mask_ref = oracle.clip_factors(nsq.astype(np.float64), C)
+    band = guard_band(np.maximum(n_ref, 1e-300), C, 1e-4)
+    np.testing.assert_array_equal(m.cpu().numpy()[~band], mask_ref[~band])
+    got = f.cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(got, c_ref, rtol=1e-6, atol=0)
+
+
+# --------------------------------------------------------- clipped sum
+
+CLIP_SHAPES = [
+    # B, T, d_in, d_out, dtype
+    (32, 1, 256, 128, wl.F32),
+    (16, 3, 40, 24, wl.F32),
+    (8, 64, 136, 200, wl.BF16),     # per-example steps, rescaled accumulator
+    (6, 100, 72, 48, wl.BF16),      # T not a multiple of the K step (zero-padded rows)
+    (12, 5, 64, 96, wl.BF16),       # small T: weight applied to the operand
+    (4, 70, 13, 21, wl.BF16),       # non-vector loads
+    (3, 9, 11, 7, wl.F32),
+]
+
+
+def _clip_case(dp, shape, C, accumulate=False):
+    import torch
+    B, T, d_in, d_out, dtype = shape
+    h = _host_layer(B, T, d_in, d_out, dtype, seed=B * 7 + T, g_scale=0.05)
+    (L, A, G), = device_layers([h])
+    ol = oracle_layers([h])
+    nsq_ref = oracle.per_example_norms_sq(ol)
+    nsq = torch.from_numpy(nsq_ref.astype(np.float32)).cuda()
+    grad = torch.full((d_out, d_in), 0.5, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(dp.dpsgd_clip_workspace_bytes(L), 1), dtype=torch.uint8, device="cuda")
+    f = torch.empty(B, dtype=torch.float32, device="cuda")
+    m = torch.empty(B, dtype=torch.uint8, device="cuda")
+    dp.dpsgd_clip_accumulate(L, nsq, C, grad, accumulate=accumulate, factors_out=f, mask_out=m,
+                             workspace=ws)
+    _sync()
+    # The oracle takes the same float32 squared norms the GPU was given.
+    n_ref, c_ref, mask_ref = oracle.clip_factors(nsq_ref.astype(np.float32).astype(np.float64), C)
+    S_ref = oracle.clipped_sum(ol[0], c_ref) + (0.5 if accumulate else 0.0)
+    return h, torch_to_float64(grad), S_ref, m.cpu().numpy(), mask_ref, n_ref
+
+
+@pytest.mark.parametrize("shape", CLIP_SHAPES)
+def test_clip_sum_matches_oracle(dp, shape):
+    dtype = shape[4]
+    # C chosen inside the spread of norms so both clipped and unclipped examples occur.
+    _, _, _, _, _, n0 = _clip_case(dp, shape, math.inf)
+    C = float(np.median(n0))
+    h, got, ref, mask, mask_ref, n_ref = _clip_case(dp, shape, C)
+    band = guard_band(n_ref, C, TOL[dtype])
+    np.testing.assert_array_equal(mask[~band], mask_ref[~band])
+    r = assert_sum_close(got, ref, TOL[dtype], "clipped sum")
+    _log(f"clip sum rel err {r:.2e}")
+    B, T = shape[0], shape[1]
+    if dtype == wl.F32 or (T >= 64 and (-T) % 64 * 8 <= T):
+        assert r <= 2e-5        # weights applied in fp32
+    else:
+        assert r <= 5e-3        # one bf16 rounding of c_i * G
+
+
+@pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2]])
+def test_clip_sum_accumulates(dp, shape):
+    h, got, ref, *_ = _clip_case(dp, shape, 1.0, accumulate=True)
+    assert_sum_close(got, ref, TOL[shape[4]], "accumulated clipped sum")
+
+
+@pytest.mark.parametrize("shape", [CLIP_SHAPES[1], CLIP_SHAPES[2]])
+def test_unclipped_sum_is_batch_gradient(dp, shape):
+    h, got, ref, mask, *_ = _clip_case(dp, shape, math.inf)
+    assert not mask.any()
+    A = wl.to_float64(h.A, h.dtype)
+    G = wl.to_float64(h.G, h.dtype)
+    batch = G.reshape(-1, h.d_out).T @ A.reshape(-1, h.d_in)
+    assert_sum_close(got, batch, 1e-5, "batch gradient")
+
+
+# ------------------------------------------------------------- whole step
+
+
+def _run_step(dp, wname, B=None, T=None, scale=1.0):
+    import torch
+    W = wl.WORKLOADS[wname]
+    hs = wl.make_layers_numpy(W, B=B, T=T)
+    dl = device_layers(hs)
+    Ls = [x[0] for x in dl]
+    buf = dp.alloc_step(Ls)
+    dp.run_step(Ls, buf, W.C, W.sigma, W.noise_seed, W.step, scale)
+    _sync()
+    return W, hs, buf
+
+
+@pytest.mark.parametrize("wname,B,T", [("c1", None, None), ("c2", None, None),
+                                       ("c3", 8, 512), ("c4", 2, 256), ("c5", 4, 64)])
+def test_step_matches_oracle(dp, wname, B, T):
+    W, hs, buf = _run_step(dp, wname, B, T, scale=1.0 / (B or wl.WORKLOADS[wname].B))
+    res = oracle.dpsgd_step(oracle_layers(hs), W.C, W.sigma, W.noise_seed, W.step,
+                            scale=1.0 / (B or W.B))
+    tol = TOL[W.dtype]
+    n_gpu = np.sqrt(torch_to_float64(buf.norms_sq))
+    assert float(np.max(np.abs(n_gpu - res.norms) / res.norms)) <= min(tol, 1e-4)
+    band = guard_band(res.norms, W.C, tol)
+    np.testing.assert_array_equal(buf.mask.cpu().numpy()[~band], res.mask[~band])
+    for k, g in enumerate(buf.grads):
+        assert_sum_close(torch_to_float64(g), res.noised[k], tol, f"layer {k} noised output")
+    # Structural invariant of the verifier: the averaged clipped sum has norm <= C.
+    # (checked on the noise-free sums below)
+
+
+def test_structural_norm_invariant(dp):
+    import torch
+    W = wl.WORKLOADS["c3"]
+    hs = wl.make_layers_numpy(W, B=8, T=512)
+    dl = device_layers(hs)
+    Ls = [x[0] for x in dl]
+    buf = dp.alloc_step(Ls)
+    dp.dpsgd_per_example_norms_multi(Ls, 0, buf.norms_sq, workspace=buf.norms_ws)
+    dp.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, workspace=buf.clip_ws)
+    _sync()
+    total = math.sqrt(sum(float(torch.sum(g.double() ** 2)) for g in buf.grads))
+    assert total / 8 <= W.C * (1 + 1e-4)
+
+
+def test_determinism(dp):
+    """Two runs of the same step give bitwise-identical norms and outputs."""
+    import torch
+    W = wl.WORKLOADS["c5"]
+    hs = wl.make_layers_numpy(W, B=4, T=64)
+    Ls = [x[0] for x in device_layers(hs)]
+    outs = []
+    for _ in range(2):
+        buf = dp.alloc_step(Ls)
+        dp.run_step(Ls, buf, W.C, W.sigma, W.noise_seed, W.step, 0.25)
+        _sync()
+        outs.append(buf)
+    assert torch.equal(outs[0].norms_sq, outs[1].norms_sq)
+    for a, b in zip(outs[0].grads, outs[1].grads):
+        assert torch.equal(a, b)
+
+
+def test_microbatch_accumulation(dp):
+    """Two half-batches with accumulate=1 give the one-batch clipped sum."""
+    import torch
+    W = wl.WORKLOADS["c3"]
+    h = wl.make_layers_numpy(W, B=8, T=128)[0]
+    full = device_layers([h])[0]
+    halves = []
+    for lo in (0, 4):
+        hh = wl.HostLayer(A=h.A[lo:lo + 4].copy(), G=h.G[lo:lo + 4].copy(), d_in=h.d_in,
+                          d_out=h.d_out, tensor_id=0, dtype=h.dtype)
+        halves.append(device_layers([hh])[0])
+    grad_full = torch.empty((h.d_out, h.d_in), dtype=torch.float32, device="cuda")
+    grad_mb = torch.empty_like(grad_full)
+    for k, (L, A, G) in enumerate([full] + halves):
+        nsq = torch.empty(L.B, dtype=torch.float32, device="cuda")
+        ws = torch.empty(dp.dpsgd_norms_workspace_bytes(L), dtype=torch.uint8, device="cuda")
+        dp.dpsgd_per_example_norms(L, 0, nsq, workspace=ws)
+        cws = torch.empty(dp.dpsgd_clip_workspace_bytes(L), dtype=torch.uint8, device="cuda")
+        if k == 0:
+            dp.dpsgd_clip_accumulate(L, nsq, W.C, grad_full, workspace=cws)
+        else:
+            dp.dpsgd_clip_accumulate(L, nsq, W.C, grad_mb, accumulate=k == 2, workspace=cws)
+    _sync()
+    assert rel_err(torch_to_float64(grad_mb), torch_to_float64(grad_full)) <= 1e-5
