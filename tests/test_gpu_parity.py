@@ -179,7 +179,8 @@ def test_clip_factors_and_mask_exact(dp):
     rng = np.random.default_rng(5)
     n = np.concatenate([rng.uniform(0.01, 0.99, 100), rng.uniform(1.01, 50, 100),
                         [0.0, 1e-30, 1e30]])
-    nsq = (n * n).astype(np.float32)
+    with np.errstate(over="ignore"):
+        nsq = (n * n).astype(np.float32)   # 1e30^2 overflows to +inf on purpose
     t = torch.from_numpy(nsq).cuda()
     f = torch.empty_like(t)
     m = torch.empty(len(n), dtype=torch.uint8, device="cuda")
@@ -312,7 +313,8 @@ def test_determinism(dp):
     import torch
     W = wl.WORKLOADS["c5"]
     hs = wl.make_layers_numpy(W, B=4, T=64)
-    Ls = [x[0] for x in device_layers(hs)]
+    dl = device_layers(hs)  # keeps the input tensors alive while the descriptors are used
+    Ls = [x[0] for x in dl]
     outs = []
     for _ in range(2):
         buf = dp.alloc_step(Ls)
