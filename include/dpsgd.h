@@ -58,7 +58,7 @@ typedef enum dpsgd_norm_mode {
 
 typedef enum dpsgd_status {
   DPSGD_OK = 0,
-  DPSGD_ERR_INVALID_ARG = -1,  /* null required pointer, size < 1 or overflow, C <= 0 or NaN,
+  DPSGD_ERR_INVALID_ARG = -1,  /* null or misaligned required pointer, size < 1 or overflow, C <= 0 or NaN,
                                   sigma < 0 or NaN, scale not finite                      */
   DPSGD_ERR_UNSUPPORTED = -2,  /* unknown dtype or mode, mixed dtypes in one call         */
   DPSGD_ERR_WORKSPACE = -3,    /* workspace NULL or smaller than the *_workspace_bytes value */
@@ -68,8 +68,9 @@ typedef enum dpsgd_status {
 /* One linear layer y = x W^T (W: [d_out][d_in]) as seen by one batch.
  * Paper: Section 2.2, per-example gradient of the trainable parameters. */
 typedef struct dpsgd_layer {
-  const void* A;       /* [B][T][d_in]  activations, dtype                       */
-  const void* G;       /* [B][T][d_out] output gradients dloss_i/dy_t, dtype     */
+  const void* A;       /* [B][T][d_in]  activations, dtype; 16-byte aligned      */
+  const void* G;       /* [B][T][d_out] output gradients dloss_i/dy_t, dtype;
+                          16-byte aligned                                         */
   int64_t B;           /* examples in the batch, >= 1                            */
   int64_t T;           /* positions per example (sequence length), >= 1          */
   int64_t d_in;        /* >= 1                                                   */

@@ -31,6 +31,7 @@ int check_layer(const dpsgd_layer* L, bool data) {
     return DPSGD_ERR_INVALID_ARG;
   if (L->d_out > (INT64_C(1) << 40) / L->d_in) return DPSGD_ERR_INVALID_ARG;
   if (data && (!L->A || !L->G)) return DPSGD_ERR_INVALID_ARG;
+  if (data && (!aligned16(L->A) || !aligned16(L->G))) return DPSGD_ERR_INVALID_ARG;
   return DPSGD_OK;
 }
 

@@ -73,6 +73,16 @@ int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
                  float* norms_sq, int accumulate, float* partials, int64_t P,
                  const int64_t* cols, hipStream_t stream);
 
+// 256x256-tile bf16 kernels (gemm_tr.hip): eligibility (bf16, d_in and d_out
+// multiples of 256, T a multiple of 32), K slices of a layer, launchers.
+bool tr_tile_ok(const dpsgd_layer& L);
+int64_t tr_q_total(const dpsgd_layer& L);
+int launch_tr_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
+                   float* const* outs, const int* splits, const int* accumulate,
+                   hipStream_t stream);
+int launch_tr_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                        float* partials, int64_t P, hipStream_t stream);
+
 // Materialised-norm partials (gemm.hip) for the layers idx[0..n).
 int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream);

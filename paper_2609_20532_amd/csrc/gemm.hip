@@ -371,10 +371,11 @@ int64_t clip_q_total(const dpsgd_layer& L, int scale) {
   return scale == SCALE_ACC ? L.B * ceil_div(L.T, bk) : ceil_div(L.B * L.T, bk);
 }
 
+// Every row starts 16-byte aligned (the ABI requires aligned A and G).
 template <typename TIn>
 bool tgemm_vec_ok(const dpsgd_layer& L) {
   constexpr int E = TileCfg<TIn>::E;
-  return aligned16(L.A) && aligned16(L.G) && L.d_in % E == 0 && L.d_out % E == 0;
+  return L.d_in % E == 0 && L.d_out % E == 0;
 }
 
 template <typename TIn, bool VEC, int SCALE, int EPI>
@@ -425,17 +426,23 @@ int launch_tgemm_group(const dpsgd_layer* layers, const int* idx, int n, const f
 
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // Split along K only when the layers of the call together have too few
-  // output tiles to occupy the GPU (two resident workgroups on 256 CUs).
-  constexpr int64_t kTargetWGs = 512;
-  int64_t total_tiles = 0;
-  for (int l = 0; l < n_layers; ++l)
-    total_tiles += ceil_div(layers[l].d_out, kTile) * ceil_div(layers[l].d_in, kTile);
-  const int64_t want = total_tiles >= kTargetWGs ? 1 : ceil_div(kTargetWGs, total_tiles);
+  // output tiles to occupy the GPU: one resident 256-tile workgroup per CU, or
+  // two 128-tile workgroups per CU, on 256 CUs. Each kernel kind has its own
+  // launch, so each is planned on its own tiles.
+  int64_t tiles_big = 0, tiles_small = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    const dpsgd_layer& L = layers[l];
+    if (tr_tile_ok(L)) tiles_big += (L.d_out / 256) * (L.d_in / 256);
+    else tiles_small += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+  }
+  const int64_t want_big = tiles_big >= 256 ? 1 : ceil_div(256, tiles_big > 0 ? tiles_big : 1);
+  const int64_t want_small = tiles_small >= 512 ? 1 : ceil_div(512, tiles_small > 0 ? tiles_small : 1);
   size_t off = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
-    const int64_t q_total = clip_q_total(L, clip_scale_mode(L));
-    int64_t s = want;
+    const bool big = tr_tile_ok(L);
+    const int64_t q_total = big ? tr_q_total(L) : clip_q_total(L, clip_scale_mode(L));
+    int64_t s = big ? want_big : want_small;
     if (s > q_total / 4) s = q_total / 4;  // at least 4 K steps per split
     if (s < 1) s = 1;
     if (s > 64) s = 64;
@@ -451,15 +458,15 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
                     hipStream_t stream) {
   // Group layers by kernel variant; each group is one grouped launch.
   const bool bf16 = layers[0].dtype == DPSGD_BF16;
-  int idx[4][kMaxLayersPerLaunch];
-  float* outs[4][kMaxLayersPerLaunch];
-  int spl[4][kMaxLayersPerLaunch];
-  int acc[4][kMaxLayersPerLaunch];
-  int cnt[4] = {0, 0, 0, 0};
+  int idx[5][kMaxLayersPerLaunch];
+  float* outs[5][kMaxLayersPerLaunch];
+  int spl[5][kMaxLayersPerLaunch];
+  int acc[5][kMaxLayersPerLaunch];
+  int cnt[5] = {0, 0, 0, 0, 0};
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
-    const int g = (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
+    const int g = tr_tile_ok(L) ? 4 : (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
     const int k = cnt[g]++;
     idx[g][k] = l;
     spl[g][k] = plan.splits[l];
@@ -470,6 +477,7 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
     acc[g][k] = accumulate;
   }
   int st = DPSGD_OK;
+  if (cnt[4]) st = launch_tr_clip(layers, idx[4], cnt[4], factors, outs[4], spl[4], acc[4], stream);
 #define DPSGD_TG(T_, V_, S_, g_)                                                                \
   if (st == DPSGD_OK && cnt[g_])                                                               \
   st = launch_tgemm_group<T_, V_, S_, EPI_STORE>(layers, idx[g_], cnt[g_], factors, outs[g_], \
@@ -513,13 +521,17 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
 int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream) {
   const bool bf16 = layers[idx[0]].dtype == DPSGD_BF16;
-  int iv[256], is[256], nv = 0, ns = 0;
+  int iv[256], is[256], ib[256], nv = 0, ns = 0, nb = 0;
   for (int k = 0; k < n; ++k) {
     const dpsgd_layer& L = layers[idx[k]];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
-    if (vec) iv[nv++] = idx[k]; else is[ns++] = idx[k];
+    if (tr_tile_ok(L)) ib[nb++] = idx[k];
+    else if (vec) iv[nv++] = idx[k];
+    else is[ns++] = idx[k];
   }
   int st = DPSGD_OK;
+  if (nb) st = launch_tr_mat_norms(layers, ib, nb, cols, partials, P, stream);
+  if (st != DPSGD_OK) return st;
   if (bf16) {
     if (nv) st = launch_tgemm_group<uint16_t, true, SCALE_NONE, EPI_SUMSQ>(
                 layers, iv, nv, nullptr, nullptr, nullptr, nullptr, cols, partials, P, stream);

@@ -110,6 +110,65 @@ __device__ __forceinline__ void mma_step(const float* __restrict__ As, const flo
   }
 }
 
+// Generic bf16 wave tile: acc[MB][NB] += As[MB*16 rows] . Bs[NB*16 rows]^T over one
+// K step of BK = 64 in LDS (same operand and output layout as mma_step above).
+// With RESCALE, every accumulator block is multiplied by `s` just before its
+// first MFMA of the step, so only a few blocks are in flight in VGPRs at a time.
+template <int MB, int NB, bool RESCALE = false>
+__device__ __forceinline__ void mma_tile_bf16(const uint16_t* __restrict__ As,
+                                              const uint16_t* __restrict__ Bs,
+                                              f32x4_t (&acc)[MB][NB], int lane, float s = 1.0f) {
+  constexpr int SK = TileCfg<uint16_t>::SK;
+  const int r = lane & 15;
+  const int ko = (lane >> 4) * 8;
+#pragma unroll
+  for (int kc = 0; kc < TileCfg<uint16_t>::BK / 32; ++kc) {
+    bf16x8_t b[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      b[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (j * 16 + r) * SK + kc * 32 + ko);
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(As + (i * 16 + r) * SK + kc * 32 + ko);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const f32x4_t c = (RESCALE && kc == 0) ? acc[i][j] * s : acc[i][j];
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[j], c, 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int MB, int NB>
+__device__ __forceinline__ void zero_acc_t(f32x4_t (&acc)[MB][NB]) {
+#pragma unroll
+  for (int i = 0; i < MB; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+}
+
+// Multiplies the accumulators by s one block row at a time; the scheduling
+// barriers keep the compiler from reading every accumulator register into
+// VGPRs at once (the accumulators of large wave tiles live in AGPRs).
+template <int MB, int NB>
+__device__ __forceinline__ void scale_acc_t(f32x4_t (&acc)[MB][NB], float s) {
+#pragma unroll
+  for (int i = 0; i < MB; ++i) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[i][j] *= s;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Workgroup index remapped so that consecutive logical indices run on the same
+// XCD. Workgroups are dispatched round-robin over the 8 XCDs (workgroup b to
+// XCD b % 8); this gives XCD x the contiguous logical range of its share, so
+// tiles that read the same operand rows share that XCD's L2.
+__device__ __forceinline__ uint32_t xcd_logical_index(uint32_t bid, uint32_t nwg) {
+  const uint32_t per = nwg >> 3, rem = nwg & 7u, xcd = bid & 7u, idx = bid >> 3;
+  return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+}
+
 // Element loads for the non-vector paths.
 __device__ __forceinline__ float load_elem(const uint16_t* p) { return bf16_to_f32(*p); }
 __device__ __forceinline__ float load_elem(const float* p) { return *p; }

@@ -290,10 +290,11 @@ int launch_ghost_group(const dpsgd_layer* layers, const int* idx, int n, const i
   return DPSGD_OK;
 }
 
+// Every row starts 16-byte aligned (the ABI requires aligned A and G).
 template <typename TIn>
 bool ghost_vec_ok(const dpsgd_layer& L) {
   constexpr int E = TileCfg<TIn>::E;
-  return aligned16(L.A) && aligned16(L.G) && L.d_in % E == 0 && L.d_out % E == 0;
+  return L.d_in % E == 0 && L.d_out % E == 0;
 }
 
 template <typename TIn>
@@ -353,7 +354,9 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
       const int64_t nt = ceil_div(L.T, kTile);
       return nt * (nt + 1) / 2;
     }
-    default: return ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+    default:
+      if (tr_tile_ok(L)) return (L.d_out / 256) * (L.d_in / 256);
+      return ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
   }
 }
 

@@ -73,6 +73,7 @@ def _lay(**kw):
     (dict(B=0), -1), (dict(T=0), -1), (dict(d_in=-3), -1), (dict(d_out=0), -1),
     (dict(A=None), -1), (dict(G=None), -1), (dict(dtype=7), -2),
     (dict(B=1 << 40), -1), (dict(d_in=1 << 31, d_out=1 << 31), -1),
+    (dict(A=24), -1), (dict(G=40), -1),   # not 16-byte aligned
 ])
 def test_norms_rejects_bad_layers(lib, kw, status):
     L = _lay(**kw)

@@ -114,6 +114,7 @@ NORM_SHAPES = [
     (2, 300, 64, 264),     # three T tiles
     (2, 64, 300, 10),      # d_out < 16
     (2, 40, 13, 21),       # d not a multiple of the vector width
+    (2, 128, 256, 512),    # 256x256-tile kernel (bf16: d multiples of 256, T of 64)
 ]
 
 
@@ -204,7 +205,18 @@ CLIP_SHAPES = [
     (12, 5, 64, 96, wl.BF16),       # small T: weight applied to the operand
     (4, 70, 13, 21, wl.BF16),       # non-vector loads
     (3, 9, 11, 7, wl.F32),
+    (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
+    (8, 256, 256, 256, wl.BF16),    # 256x256-tile kernel, split along K
 ]
+
+
+def _weights_in_fp32(shape):
+    """True when the clip weight is applied in fp32 (no bf16 rounding of c_i * G)."""
+    B, T, d_in, d_out, dtype = shape
+    if dtype == wl.F32:
+        return True
+    big = d_in % 256 == 0 and d_out % 256 == 0 and T % 64 == 0
+    return not big and T >= 64 and (-T) % 64 * 8 <= T
 
 
 def _clip_case(dp, shape, C, accumulate=False):
@@ -239,8 +251,7 @@ def test_clip_sum_matches_oracle(dp, shape):
     np.testing.assert_array_equal(mask[~band], mask_ref[~band])
     r = assert_sum_close(got, ref, TOL[dtype], "clipped sum")
     _log(f"clip sum rel err {r:.2e}")
-    B, T = shape[0], shape[1]
-    if dtype == wl.F32 or (T >= 64 and (-T) % 64 * 8 <= T):
+    if _weights_in_fp32(shape):
         assert r <= 2e-5        # weights applied in fp32
     else:
         assert r <= 5e-3        # one bf16 rounding of c_i * G
