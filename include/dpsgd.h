@@ -130,7 +130,7 @@ int dpsgd_clip_factors(const float* norms_sq, int64_t B, float C, float* factors
  * (device, optional) receive c and the clip mask. The _multi form does the
  * same for n_layers layers (one grad buffer each, all with the same B) in one
  * grouped launch. workspace: at least dpsgd_clip_workspace_bytes(...) bytes.
- * grad must not alias any input.
+ * grad must be 16-byte aligned and must not alias any input.
  * ------------------------------------------------------------------------- */
 size_t dpsgd_clip_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers);
 

@@ -156,7 +156,7 @@ int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
   if (st != DPSGD_OK) return st;
   if (!norms_sq || !grads) return DPSGD_ERR_INVALID_ARG;
   for (int32_t l = 0; l < n_layers; ++l)
-    if (!grads[l]) return DPSGD_ERR_INVALID_ARG;
+    if (!grads[l] || !aligned16(grads[l])) return DPSGD_ERR_INVALID_ARG;
   if (bad_float(C) || !(C > 0.0f)) return DPSGD_ERR_INVALID_ARG;
   const size_t need = clip_ws_bytes(layers, n_layers);
   if (!workspace || workspace_bytes < need) return DPSGD_ERR_WORKSPACE;

@@ -77,8 +77,17 @@ int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
 // multiples of 256, T a multiple of 32), K slices of a layer, launchers.
 bool tr_tile_ok(const dpsgd_layer& L);
 int64_t tr_q_total(const dpsgd_layer& L);
+int tr_cu_count();
+
+// Work split of one clip launch over the 256-tile kernel: whole tiles for the
+// full rounds over the CUs, the last round's K slices spread over tail workers.
+struct TrClipPlan {
+  int64_t n_tiles = 0, n_full = 0, n_tail = 0, Q = 0;
+  size_t tail_bytes = 0;  // tail partials in the workspace
+};
+void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan);
 int launch_tr_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
-                   float* const* outs, const int* splits, const int* accumulate,
+                   float* const* outs, int accumulate, const TrClipPlan& plan, float* tail_ws,
                    hipStream_t stream);
 int launch_tr_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                         float* partials, int64_t P, hipStream_t stream);
@@ -94,7 +103,9 @@ int launch_clip_factors(const float* norms_sq, int64_t B, float C, float* factor
 struct ClipPlan {
   int splits[kMaxLayersPerLaunch];
   size_t partial_offset[kMaxLayersPerLaunch];  // bytes from the partial base
-  size_t partial_bytes;                          // total
+  size_t partial_bytes;                          // total (split partials + 256-tile tail)
+  TrClipPlan tr;                                 // layers on the 256-tile kernel
+  size_t tr_offset;                              // their tail partials, from the partial base
 };
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan);
 

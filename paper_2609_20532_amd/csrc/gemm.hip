@@ -425,32 +425,38 @@ int launch_tgemm_group(const dpsgd_layer* layers, const int* idx, int n, const f
 }  // namespace
 
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
-  // Split along K only when the layers of the call together have too few
-  // output tiles to occupy the GPU: one resident 256-tile workgroup per CU, or
-  // two 128-tile workgroups per CU, on 256 CUs. Each kernel kind has its own
-  // launch, so each is planned on its own tiles.
-  int64_t tiles_big = 0, tiles_small = 0;
+  // Layers on the 256-tile kernel are balanced by its own plan (whole tiles,
+  // then a split tail). The 128-tile layers are split along K only when they
+  // have too few output tiles to occupy the GPU (two workgroups per CU).
+  const int cus = tr_cu_count();
+  int tr_idx[kMaxLayersPerLaunch], n_tr = 0;
+  int64_t tiles_small = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
-    if (tr_tile_ok(L)) tiles_big += (L.d_out / 256) * (L.d_in / 256);
+    if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
     else tiles_small += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
   }
-  const int64_t want_big = tiles_big >= 256 ? 1 : ceil_div(256, tiles_big > 0 ? tiles_big : 1);
-  const int64_t want_small = tiles_small >= 512 ? 1 : ceil_div(512, tiles_small > 0 ? tiles_small : 1);
+  const int64_t target = 2 * (int64_t)cus;
+  const int64_t want_small =
+      tiles_small >= target ? 1 : ceil_div(target, tiles_small > 0 ? tiles_small : 1);
   size_t off = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
-    const bool big = tr_tile_ok(L);
-    const int64_t q_total = big ? tr_q_total(L) : clip_q_total(L, clip_scale_mode(L));
-    int64_t s = big ? want_big : want_small;
-    if (s > q_total / 4) s = q_total / 4;  // at least 4 K steps per split
-    if (s < 1) s = 1;
-    if (s > 64) s = 64;
+    int64_t s = 1;
+    if (!tr_tile_ok(L)) {
+      const int64_t q_total = clip_q_total(L, clip_scale_mode(L));
+      s = want_small;
+      if (s > q_total / 4) s = q_total / 4;  // at least 4 K steps per split
+      if (s < 1) s = 1;
+      if (s > 64) s = 64;
+    }
     plan->splits[l] = (int)s;
     plan->partial_offset[l] = off;
     if (s > 1) off += round_up((size_t)s * (size_t)L.d_out * (size_t)L.d_in * sizeof(float), 256);
   }
-  plan->partial_bytes = off;
+  plan_tr_clip(layers, tr_idx, n_tr, cus, &plan->tr);
+  plan->tr_offset = off;
+  plan->partial_bytes = off + round_up(plan->tr.tail_bytes, 256);
 }
 
 int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factors,
@@ -477,7 +483,11 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
     acc[g][k] = accumulate;
   }
   int st = DPSGD_OK;
-  if (cnt[4]) st = launch_tr_clip(layers, idx[4], cnt[4], factors, outs[4], spl[4], acc[4], stream);
+  if (cnt[4])
+    st = launch_tr_clip(layers, idx[4], cnt[4], factors, outs[4], accumulate, plan.tr,
+                        reinterpret_cast<float*>(reinterpret_cast<char*>(partial_base) +
+                                                 plan.tr_offset),
+                        stream);
 #define DPSGD_TG(T_, V_, S_, g_)                                                                \
   if (st == DPSGD_OK && cnt[g_])                                                               \
   st = launch_tgemm_group<T_, V_, S_, EPI_STORE>(layers, idx[g_], cnt[g_], factors, outs[g_], \

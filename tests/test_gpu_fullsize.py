@@ -127,8 +127,9 @@ def test_full_size_step(dp, wname, n_samples):
         assert ro <= tol, f"layer {li}: noised output rel err {ro:.2e}"
         worst_sum, worst_noised = max(worst_sum, rs), max(worst_noised, ro)
     _log(f"clipped sum worst rel err {worst_sum:.2e}; noised worst rel err {worst_noised:.2e}")
-    # One bf16 rounding of c_i * G per term (relative <= 2^-9): far inside the bf16 gate.
-    assert worst_sum <= 5e-3
+    # The clip weights are applied in fp32: only fp32 summation order separates
+    # the sums from the float64 definition.
+    assert worst_sum <= 1e-4
     # Structural invariant (paper, verifier): the averaged clipped sum has norm <= C.
     total = math.sqrt(sum(float(torch.sum(s.double() ** 2)) for s in sums))
     assert total / W.B <= W.C * (1 + 1e-4)
