@@ -82,7 +82,7 @@ int tr_cu_count();
 // Work split of one clip launch over the 256-tile kernel: whole tiles for the
 // full rounds over the CUs, the last round's K slices spread over tail workers.
 struct TrClipPlan {
-  int64_t n_tiles = 0, n_full = 0, n_tail = 0, Q = 0;
+  int64_t n_tiles = 0, n_full = 0, n_tail = 0, Q = 0, tail_w = 1;
   size_t tail_bytes = 0;  // tail partials in the workspace
 };
 void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan);

@@ -257,6 +257,32 @@ def test_clip_sum_matches_oracle(dp, shape):
         assert r <= 5e-3        # one bf16 rounding of c_i * G
 
 
+@pytest.mark.parametrize("shape", [CLIP_SHAPES[2], CLIP_SHAPES[-2], CLIP_SHAPES[-1]])
+def test_zero_factor_examples_contribute_nothing(dp, shape):
+    """An example whose squared norm is +inf gets factor C/inf = 0; with finite
+    inputs its clipped gradient 0 * g_i is exactly zero (Section 2.2)."""
+    import torch
+    B, T, d_in, d_out, dtype = shape
+    h = _host_layer(B, T, d_in, d_out, dtype, seed=B * 11 + T, g_scale=0.05)
+    (L, A, G), = device_layers([h])
+    ol = oracle_layers([h])
+    nsq_ref = oracle.per_example_norms_sq(ol).astype(np.float32)
+    nsq_ref[1] = np.inf
+    nsq_ref[B - 1] = np.inf
+    C = float(np.median(np.sqrt(nsq_ref[np.isfinite(nsq_ref)])))
+    nsq = torch.from_numpy(nsq_ref).cuda()
+    grad = torch.zeros((d_out, d_in), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(dp.dpsgd_clip_workspace_bytes(L), 1), dtype=torch.uint8, device="cuda")
+    f = torch.empty(B, dtype=torch.float32, device="cuda")
+    dp.dpsgd_clip_accumulate(L, nsq, C, grad, factors_out=f, workspace=ws)
+    _sync()
+    _, c_ref, _ = oracle.clip_factors(nsq_ref.astype(np.float64), C)
+    assert c_ref[1] == 0.0 and c_ref[B - 1] == 0.0
+    assert f.cpu().numpy()[1] == 0.0 and f.cpu().numpy()[B - 1] == 0.0
+    ref = oracle.clipped_sum(ol[0], c_ref)
+    assert_sum_close(torch_to_float64(grad), ref, TOL[dtype], "clipped sum with zero factors")
+
+
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2], CLIP_SHAPES[-1]])
 def test_clip_sum_accumulates(dp, shape):
     h, got, ref, *_ = _clip_case(dp, shape, 1.0, accumulate=True)
