@@ -75,6 +75,11 @@ int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
 
 // 256x256-tile bf16 kernels (gemm_tr.hip): eligibility (bf16, d_in and d_out
 // multiples of 256, T a multiple of 32), K slices of a layer, launchers.
+// Gram-form norms with direct LDS loads (ghost.hip): bf16, widths % 64 == 0.
+bool ghost_dma_ok(const dpsgd_layer& L);
+int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                     float* partials, int64_t P, hipStream_t stream);
+
 bool tr_tile_ok(const dpsgd_layer& L);
 int64_t tr_q_total(const dpsgd_layer& L);
 int tr_cu_count();

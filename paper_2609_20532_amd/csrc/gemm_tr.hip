@@ -26,6 +26,7 @@
 // kept in units of the current example's factor and multiplied by
 // c_prev / c_next at each example boundary
 // (paper: Section 2.2, g_bar_i = c_i g_i summed over the batch).
+#include "lds_dma.h"
 #include "mma.h"
 
 namespace dpsgd {
@@ -88,31 +89,6 @@ __device__ const uint4 kZeroRow[32] = {};
 __host__ __device__ constexpr int block_offset(int j) {
   return j * kTrBlockStride + 32 * ((j & 3) + 4 * ((j >> 3) & 1));
 }
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Workgroup barrier that also orders the compiler's memory accesses (LDS
-// reads cannot move across it) without making the hardware wait for
-// outstanding loads, which the explicit vmcnt waits already account for.
-__device__ __forceinline__ void barrier_no_wait() { asm volatile("s_barrier" ::: "memory"); }
-
-// One 16-byte-per-lane copy from global memory into LDS at lds_addr + 16 * lane:
-// lane i reads base + voff_i (base uniform, in SGPRs; voff a 32-bit byte offset).
-// Issued as inline assembly so the compiler does not treat later LDS reads as
-// aliasing an in-flight copy (it would otherwise wait for every outstanding
-// copy before each read); completion is tracked with explicit vmcnt waits.
-__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(voff), "s"(base), "s"(lds_addr)
-               : "m0", "memory");
-}
-
 
 // MFMA operand (8 consecutive k of one row) from two transposed 8-byte reads at
 // p0 + off (k 0..3) and p1 + off (k 4..7); off is a compile-time immediate.

@@ -1,0 +1,443 @@
+// Ghost-norm (Gram form) kernels for bf16 layers whose widths are multiples
+// of 64 (paper: Section 2.2, per-example clipping by the L2 norm of g_i; the
+// squared Frobenius norm of g_i = G_i^T A_i equals <A_i A_i^T, G_i G_i^T>_F).
+//
+// A workgroup owns one example i and one 128 x 128 tile (p, q), p <= q, of
+// the T x T upper triangle (or, see below, three of them). It accumulates the
+// activation Gram tile
+//   GA[t][s] = sum_j A_i[128p + t][j] A_i[128q + s][j]   over the d_in columns
+// and then the output-gradient Gram tile GG over the d_out columns, both in
+// registers with the same layout, and returns sum_{t,s} GA[t][s] GG[t][s]
+// (times 2 off the diagonal). Rows past T are read as a copy of the last row
+// (in-bounds) and masked out of the sum.
+//
+// The contraction runs along the contiguous dimension of A and G, so the
+// MFMA operand (8 consecutive columns of one row) is a plain 16-byte LDS
+// read: slices of 32 columns of the p and q row blocks are copied from HBM
+// straight into LDS (global_load_lds_dwordx4, a four-slot ring, three slices
+// in flight) and multiplied with v_mfma_f32_32x32x16_bf16. In LDS a row takes
+// 64 bytes and its 16-byte chunk c sits at slot c ^ ((row >> 2) & 3), which
+// makes the 16-lane operand reads conflict-free; the copies choose which
+// global chunk each lane fetches accordingly.
+//
+// The pass is close to HBM-bound: every element of A and G takes part in only
+// 128 (or 256) multiply-adds per tile. When T spans two row blocks (128 < T <=
+// 256) one workgroup owns all three tiles, (0, 0), (0, 1) and (1, 1), so each
+// row of the example is fetched once: eight waves in a 2 x 4 grid each own a
+// 64 x 32 piece of all three tiles, and slices are 64 columns wide (whole
+// 128-byte lines). Otherwise every tile has its own four-wave workgroup (2 x 2
+// grid of 64 x 64 sub-tiles, two workgroups per CU), and the tiles of one
+// example run on one XCD so the rows they share come from its L2.
+#include "lds_dma.h"
+#include "mma.h"
+
+namespace dpsgd {
+namespace {
+
+constexpr int kGhRows = 128;                        // tile edge along T
+constexpr int kGhBK = 32;                           // columns per slice
+constexpr int kGhStages = 4;
+constexpr int kGhThreads = 256;
+constexpr int kGhBlockBytes = kGhRows * kGhBK * 2;  // 8 KB: one row block of a slice
+constexpr int kGhStageBytes = 2 * kGhBlockBytes;    // p block, q block
+constexpr int kGhLdsBytes = kGhStages * kGhStageBytes;
+
+struct GhEntry {
+  const void* A;
+  const void* G;
+  int32_t d_in, d_out, T;
+  int32_t nt;          // 128-row tiles along T
+  int32_t pairs;       // nt (nt + 1) / 2
+  uint32_t wg_begin;   // first workgroup of this layer in the launch
+  int32_t partial_col;
+  int32_t groups;      // nt / 2 three-tile groups
+  int32_t singles;     // pairs - 3 groups tiles outside them
+  int32_t pad;
+};
+struct GhArgs {
+  GhEntry L[kMaxLayersPerLaunch];
+  int32_t n;
+  int64_t P;
+  float* partials;
+};
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Position of tile (p, q), p <= q, in the row-major list of the upper triangle.
+__host__ __device__ inline int pair_index(int nt, int p, int q) {
+  return p * nt - p * (p - 1) / 2 + (q - p);
+}
+// Tile (p, q) belongs to the three-tile group of row blocks 0 and 1, which
+// exists when T spans exactly two row blocks.
+__host__ __device__ inline bool in_group(int nt, int p, int q) {
+  return nt == 2 && p <= 1 && q <= 1;
+}
+
+// s_waitcnt vmcnt(per * min(later, 6)).
+template <int PER>
+__device__ __forceinline__ void wait_copies_upto6(int later) {
+  switch (later < 6 ? later : 6) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<PER>(); break;
+    case 2: wait_vmcnt<2 * PER>(); break;
+    case 3: wait_vmcnt<3 * PER>(); break;
+    case 4: wait_vmcnt<4 * PER>(); break;
+    case 5: wait_vmcnt<5 * PER>(); break;
+    default: wait_vmcnt<6 * PER>(); break;
+  }
+}
+
+// sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] of tile (p, q) of example i.
+template <bool DIAG>
+__device__ float ghost_tile(const GhEntry& E, int64_t i, int p, int q, char* lds) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int T = E.T;
+  const int rows_p = min(kGhRows, T - kGhRows * p);
+  const int rows_q = min(kGhRows, T - kGhRows * q);
+  const int nA = E.d_in / kGhBK, n = nA + E.d_out / kGhBK;
+  const char* Ab = static_cast<const char*>(E.A) + i * (int64_t)T * E.d_in * 2;
+  const char* Gb = static_cast<const char*>(E.G) + i * (int64_t)T * E.d_out * 2;
+  const uint32_t lds0 = lds_address(lds);
+
+  // Copy u of this wave moves rows 16 j .. 16 j + 15 (j = wave + 4 u) of a row
+  // block: lane l takes row 16 j + l / 4 and the global chunk that belongs in
+  // its slot l % 4.
+  constexpr int kCopies = DIAG ? 2 : 4;  // per wave per slice
+  uint32_t offA[kCopies], offG[kCopies];
+#pragma unroll
+  for (int u = 0; u < kCopies; ++u) {
+    const int blk = u < 2 ? p : q;
+    const int j = (int)wave_u + 4 * (u & 1);
+    const int rvalid = u < 2 ? rows_p : rows_q;
+    const int r = min(16 * j + (lane >> 2), rvalid - 1);
+    const int row = kGhRows * blk + r;
+    const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
+    offA[u] = (uint32_t)row * (uint32_t)E.d_in * 2u + 16u * chunk;
+    offG[u] = (uint32_t)row * (uint32_t)E.d_out * 2u + 16u * chunk;
+  }
+  auto issue = [&](int s, int slot) {
+    const bool a = s < nA;
+    const char* src = a ? Ab + (int64_t)s * kGhBK * 2 : Gb + (int64_t)(s - nA) * kGhBK * 2;
+    const uint32_t dst = lds0 + (uint32_t)slot * kGhStageBytes;
+#pragma unroll
+    for (int u = 0; u < kCopies; ++u) {
+      const int j = (int)wave_u + 4 * (u & 1);
+      copy16_to_lds(src, a ? offA[u] : offG[u], dst + (u < 2 ? 0u : (uint32_t)kGhBlockBytes) + 1024u * j);
+    }
+  };
+
+  // Operand reads: lane l supplies row (l % 32) of a 32-row block and chunk
+  // 2 st + l / 32 (k step st of the slice).
+  const int f = (lane >> 2) & 3, g = lane >> 5;
+  uint32_t rd[2];
+#pragma unroll
+  for (int st = 0; st < 2; ++st) rd[st] = (lane & 31) * 64 + 16 * ((2 * st + g) ^ f);
+  const uint32_t rowA = 64 * wm * 64, rowB = (DIAG ? 0 : kGhBlockBytes) + 64 * wn * 64;
+
+  f32x16_t accA[2][2], accG[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) accA[a][b] = accG[a][b] = f32x16_t{};
+
+  // All waves must be done with the ring before a new tile overwrites it.
+  __syncthreads();
+#pragma unroll
+  for (int d = 0; d < kGhStages - 1; ++d)
+    if (d < n) issue(d, d);
+
+  auto slice = [&](int s, f32x16_t (&acc)[2][2]) {
+    // This wave's copies of slice s have landed once at most the later
+    // slices' copies are outstanding; the barrier makes every wave's part
+    // visible and guarantees slice s - 1, whose slot is refilled next, is no
+    // longer read.
+    const int later = n - 1 - s;
+    if (later >= kGhStages - 2) wait_vmcnt<kCopies * (kGhStages - 2)>();
+    else if (later == 1) wait_vmcnt<kCopies>();
+    else wait_vmcnt<0>();
+    barrier_no_wait();
+    if (s + kGhStages - 1 < n) issue(s + kGhStages - 1, (s + kGhStages - 1) % kGhStages);
+    typedef __attribute__((address_space(3))) const bf16x8_t lds_frag;
+    const char* base = lds + (s % kGhStages) * kGhStageBytes;
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      bf16x8_t fa[2], fb[2];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        fa[b] = *(lds_frag*)(base + rowA + 2048 * b + rd[st]);
+        fb[b] = *(lds_frag*)(base + rowB + 2048 * b + rd[st]);
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+  };
+  for (int s = 0; s < nA; ++s) slice(s, accA);
+  for (int s = nA; s < n; ++s) slice(s, accG);
+
+  // Element v of block (a, b) in lane l: tile row 64 wm + 32 a + 8 (v / 4) +
+  // 4 (l / 32) + v % 4, column 64 wn + 32 b + l % 32.
+  float sum = 0.f;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int col = 64 * wn + 32 * b + (lane & 31);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = 64 * wm + 32 * a + 8 * (v >> 2) + 4 * g + (v & 3);
+        const float x = accA[a][b][v] * accG[a][b][v];
+        sum += (row < rows_p && col < rows_q) ? x : 0.f;
+      }
+    }
+  return sum;
+}
+
+__global__ __launch_bounds__(kGhThreads, 2) void ghost_dma_kernel(GhArgs args) {
+  __shared__ __attribute__((aligned(1024))) char lds[kGhLdsBytes];
+  // Consecutive logical indices (the tiles of one example) run on one XCD, so
+  // the rows that two tiles share are fetched from HBM into that XCD's L2 once.
+  const uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x);
+  int l = 0;
+  {
+    int lo = 0, hi = args.n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (args.L[mid].wg_begin <= job) lo = mid; else hi = mid - 1;
+    }
+    l = lo;
+  }
+  const GhEntry& E = args.L[l];
+  const uint32_t w = job - E.wg_begin;
+  // Jobs of a layer: example-major over the tiles outside the three-tile groups.
+  const int64_t i = w / (uint32_t)E.singles;
+  int single = (int)(w % (uint32_t)E.singles);
+  int p = 0, q = 0;
+  for (;; ++q) {
+    if (q == E.nt) { ++p; q = p; }
+    if (in_group(E.nt, p, q)) continue;
+    if (single-- == 0) break;
+  }
+  const int pr = pair_index(E.nt, p, q);
+  float s = p == q ? ghost_tile<true>(E, i, p, q, lds) : 2.0f * ghost_tile<false>(E, i, p, q, lds);
+  s = wave_sum(s);
+  __syncthreads();   // the ring is free again
+  float* red = reinterpret_cast<float*>(lds);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = s;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    args.partials[i * args.P + E.partial_col + pr] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// ------------------------------------------------------- three-tile groups
+//
+// Slices of 64 columns: every row of a slice is one whole 128-byte line of A
+// or G. In LDS a row takes 128 bytes and its 16-byte chunk c sits at slot
+// c ^ ((row >> 1) & 7), which keeps the 16-lane operand reads conflict-free.
+
+constexpr int kGgThreads = 512;
+constexpr int kGgBK = 64;
+constexpr int kGgStages = 4;
+constexpr int kGgBlockBytes = kGhRows * kGgBK * 2;   // 16 KB: one row block of a slice
+constexpr int kGgStageBytes = 2 * kGgBlockBytes;     // row blocks a = 2k and b = 2k + 1
+constexpr int kGgLdsBytes = kGgStages * kGgStageBytes;
+
+__global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args) {
+  __shared__ __attribute__((aligned(1024))) char lds[kGgLdsBytes];
+  const uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x);
+  int l = 0;
+  {
+    int lo = 0, hi = args.n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (args.L[mid].wg_begin <= job) lo = mid; else hi = mid - 1;
+    }
+    l = lo;
+  }
+  const GhEntry& E = args.L[l];
+  const uint32_t w = job - E.wg_begin;
+  const int64_t i = w / (uint32_t)E.groups;
+  const int a = 2 * (int)(w % (uint32_t)E.groups), b = a + 1;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int T = E.T;
+  const int rows_a = min(kGhRows, T - kGhRows * a);
+  const int rows_b = min(kGhRows, T - kGhRows * b);
+  const int nA = E.d_in / kGgBK, n = nA + E.d_out / kGgBK;
+  const char* Ab = static_cast<const char*>(E.A) + i * (int64_t)T * E.d_in * 2;
+  const char* Gb = static_cast<const char*>(E.G) + i * (int64_t)T * E.d_out * 2;
+  const uint32_t lds0 = lds_address(lds);
+
+  // Copy u of this wave moves rows 8 j .. 8 j + 7 (j = wave + 8 u) of the
+  // 256-row window of blocks a and b: lane l takes row 8 j + l / 8 and the
+  // global chunk that belongs in its slot l % 8. Rows past T repeat the last
+  // row (in-bounds; masked out of the sum).
+  constexpr int kCopies = 4;
+  uint32_t offA[kCopies], offG[kCopies];
+#pragma unroll
+  for (int u = 0; u < kCopies; ++u) {
+    const int j = (int)wave_u + 8 * u;
+    const int row = min(kGhRows * a + 8 * j + (lane >> 3), T - 1);
+    const int chunk = (lane & 7) ^ ((4 * (j & 1) + (lane >> 4)) & 7);
+    offA[u] = (uint32_t)row * (uint32_t)E.d_in * 2u + 16u * chunk;
+    offG[u] = (uint32_t)row * (uint32_t)E.d_out * 2u + 16u * chunk;
+  }
+  auto issue = [&](int s, int slot) {
+    const bool isA = s < nA;
+    const char* src = isA ? Ab + (int64_t)s * kGgBK * 2 : Gb + (int64_t)(s - nA) * kGgBK * 2;
+    const uint32_t dst = lds0 + (uint32_t)slot * kGgStageBytes;
+#pragma unroll
+    for (int u = 0; u < kCopies; ++u)
+      copy16_to_lds(src, isA ? offA[u] : offG[u], dst + 1024u * ((int)wave_u + 8 * u));
+  };
+
+  // Operand reads: lane l supplies row (l % 32) of a 32-row block and chunk
+  // 2 st + l / 32 of k step st (four per slice).
+  const int f = (lane >> 1) & 7, g = lane >> 5;
+  uint32_t rd[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) rd[st] = (lane & 31) * 128 + 16 * ((2 * st + g) ^ f);
+  const uint32_t rowsA = 64 * wm * 128, rowsB = kGgBlockBytes + 64 * wm * 128;
+  const uint32_t colA = 32 * wn * 128, colB = kGgBlockBytes + 32 * wn * 128;
+
+  // Tiles t = 0: (a, a), 1: (a, b), 2: (b, b); each wave: rows 64 wm .. +63
+  // (two 32-row blocks r) and columns 32 wn .. +31 of every tile.
+  f32x16_t accA[3][2], accG[3][2];
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int r = 0; r < 2; ++r) accA[t][r] = accG[t][r] = f32x16_t{};
+
+#pragma unroll
+  for (int d = 0; d < kGgStages - 1; ++d)
+    if (d < n) issue(d, d);
+
+  auto slice = [&](int s, f32x16_t (&acc)[3][2]) {
+    // This wave's copies of slice s have landed once at most the later
+    // slices' copies are outstanding; the barrier makes every wave's part
+    // visible and guarantees slice s - 1, whose slot is refilled next, is no
+    // longer read.
+    const int later = n - 1 - s;
+    if (later >= kGgStages - 2) wait_vmcnt<kCopies * (kGgStages - 2)>();
+    else if (later == 1) wait_vmcnt<kCopies>();
+    else wait_vmcnt<0>();
+    barrier_no_wait();
+    if (s + kGgStages - 1 < n) issue(s + kGgStages - 1, (s + kGgStages - 1) % kGgStages);
+    typedef __attribute__((address_space(3))) const bf16x8_t lds_frag;
+    const char* base = lds + (s % kGgStages) * kGgStageBytes;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      bf16x8_t fa[2], fb[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        fa[r] = *(lds_frag*)(base + rowsA + 4096 * r + rd[st]);
+        fb[r] = *(lds_frag*)(base + rowsB + 4096 * r + rd[st]);
+      }
+      const bf16x8_t ca = *(lds_frag*)(base + colA + rd[st]);
+      const bf16x8_t cb = *(lds_frag*)(base + colB + rd[st]);
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        acc[0][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], ca, acc[0][r], 0, 0, 0);
+        acc[1][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], cb, acc[1][r], 0, 0, 0);
+        acc[2][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[r], cb, acc[2][r], 0, 0, 0);
+      }
+    }
+  };
+  for (int s = 0; s < nA; ++s) slice(s, accA);
+  for (int s = nA; s < n; ++s) slice(s, accG);
+
+  // Element v of block r in lane l: tile row 64 wm + 32 r + 8 (v / 4) + 4 (l / 32)
+  // + v % 4, column 32 wn + l % 32.
+  float sum[3] = {0.f, 0.f, 0.f};
+  const int col = 32 * wn + (lane & 31);
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int rv = t == 2 ? rows_b : rows_a, cv = t == 0 ? rows_a : rows_b;
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = 64 * wm + 32 * r + 8 * (v >> 2) + 4 * g + (v & 3);
+        const float x = accA[t][r][v] * accG[t][r][v];
+        sum[t] += (row < rv && col < cv) ? x : 0.f;
+      }
+    sum[t] = wave_sum(sum[t]);
+  }
+  __syncthreads();   // the ring is free again
+  float* red = reinterpret_cast<float*>(lds);
+  if (lane == 0)
+#pragma unroll
+    for (int t = 0; t < 3; ++t) red[3 * wave + t] = sum[t];
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int t = threadIdx.x;
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < kGgThreads / 64; ++k) v += red[3 * k + t];
+    const int p = t == 2 ? b : a, q = t == 0 ? a : b;
+    args.partials[i * args.P + E.partial_col + pair_index(E.nt, p, q)] = t == 1 ? 2.0f * v : v;
+  }
+}
+
+}  // namespace
+
+bool ghost_dma_ok(const dpsgd_layer& L) {
+  return L.dtype == DPSGD_BF16 && L.d_in % kGgBK == 0 && L.d_out % kGgBK == 0 &&
+         L.T * L.d_in * 2 < (INT64_C(1) << 31) && L.T * L.d_out * 2 < (INT64_C(1) << 31);
+}
+
+int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                     float* partials, int64_t P, hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    GhArgs ga{}, ta{};
+    ga.n = ta.n = m;
+    ga.P = ta.P = P;
+    ga.partials = ta.partials = partials;
+    int64_t gwgs = 0, twgs = 0;
+    for (int k = 0; k < m; ++k) {
+      const dpsgd_layer& L = layers[idx[base + k]];
+      GhEntry E{};
+      E.A = L.A;
+      E.G = L.G;
+      E.d_in = (int32_t)L.d_in;
+      E.d_out = (int32_t)L.d_out;
+      E.T = (int32_t)L.T;
+      E.nt = (int32_t)ceil_div(L.T, kGhRows);
+      E.pairs = E.nt * (E.nt + 1) / 2;
+      // Three-tile groups pay off when they cover the whole triangle (two row
+      // blocks); with more blocks most tiles are off-diagonal singles anyway.
+      E.groups = E.nt == 2 ? 1 : 0;
+      E.singles = E.pairs - 3 * E.groups;
+      E.partial_col = (int32_t)cols[idx[base + k]];
+      ga.L[k] = E;
+      ta.L[k] = E;
+      ga.L[k].wg_begin = (uint32_t)gwgs;
+      ta.L[k].wg_begin = (uint32_t)twgs;
+      gwgs += L.B * (int64_t)E.groups;
+      twgs += L.B * (int64_t)E.singles;
+    }
+    if (gwgs > 0x7FFFFFFF || twgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    // A layer with no workgroups in a launch starts where the next one does;
+    // the kernels pick the last layer starting at or before their job, which
+    // is never an empty one.
+    if (gwgs > 0) {
+      hipLaunchKernelGGL(ghost_group_kernel, dim3((uint32_t)gwgs), dim3(kGgThreads), 0, stream, ga);
+      if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    }
+    if (twgs > 0) {
+      hipLaunchKernelGGL(ghost_dma_kernel, dim3((uint32_t)twgs), dim3(kGhThreads), 0, stream, ta);
+      if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    }
+  }
+  return DPSGD_OK;
+}
+
+}  // namespace dpsgd

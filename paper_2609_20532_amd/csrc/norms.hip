@@ -304,16 +304,19 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
   int idx_t1[256], n_t1 = 0;
   int idx_gv[256], n_gv = 0;
   int idx_gs[256], n_gs = 0;
+  int idx_gd[256], n_gd = 0;
   int idx_mat[256], n_mat = 0;
   for (int base = 0; base < n_layers; base += 256) {
-    n_t1 = n_gv = n_gs = n_mat = 0;
+    n_t1 = n_gv = n_gs = n_gd = n_mat = 0;
     const int m = n_layers - base < 256 ? n_layers - base : 256;
     for (int k = 0; k < m; ++k) {
       const int l = base + k;
       switch (forms[l]) {
         case FORM_T1: idx_t1[n_t1++] = l; break;
         case FORM_GHOST:
-          if (ghost_vec_ok<TIn>(layers[l])) idx_gv[n_gv++] = l; else idx_gs[n_gs++] = l;
+          if (ghost_dma_ok(layers[l])) idx_gd[n_gd++] = l;
+          else if (ghost_vec_ok<TIn>(layers[l])) idx_gv[n_gv++] = l;
+          else idx_gs[n_gs++] = l;
           break;
         default: idx_mat[n_mat++] = l; break;
       }
@@ -324,6 +327,7 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
       st = launch_ghost_group<TIn, true>(layers, idx_gv, n_gv, cols, partials, P, stream);
     if (st == DPSGD_OK && n_gs)
       st = launch_ghost_group<TIn, false>(layers, idx_gs, n_gs, cols, partials, P, stream);
+    if (st == DPSGD_OK && n_gd) st = launch_ghost_dma(layers, idx_gd, n_gd, cols, partials, P, stream);
     if (st == DPSGD_OK && n_mat)
       st = launch_mat_norms(layers, idx_mat, n_mat, cols, partials, P, stream);
     if (st != DPSGD_OK) return st;

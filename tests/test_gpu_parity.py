@@ -115,6 +115,10 @@ NORM_SHAPES = [
     (2, 64, 300, 10),      # d_out < 16
     (2, 40, 13, 21),       # d not a multiple of the vector width
     (2, 128, 256, 512),    # 256x256-tile kernel (bf16: d multiples of 256, T of 64)
+    (3, 200, 128, 192),    # bf16 Gram with direct loads: three-tile group, ragged block
+    (2, 256, 64, 128),     # three-tile group, full blocks
+    (2, 96, 192, 64),      # one diagonal tile, ragged
+    (2, 300, 64, 128),     # three row blocks: single tiles, ragged last block
 ]
 
 
