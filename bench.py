@@ -17,6 +17,7 @@ on this host on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -34,6 +35,13 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 METRIC = "DP-SGD clipped+noised grad throughput: examples/s per layer; % MFMA peak"
 
+# HBM bytes per launch of the clip GEMM measured with rocprofv3 counters; valid
+# only for the kernel sources they were taken with.
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "clip_gemm_c5_traffic.txt")
+GEMM_SOURCES = [os.path.join(HERE, "paper_2609_20532_amd", "csrc", f)
+                for f in ("gemm_tr.hip", "lds_dma.h", "mma.h", "common.h")]
+DOMINANT = "tgemm_tr_kernel<0>"
+
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
@@ -43,7 +51,32 @@ def parse():
     p.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-examples", type=int, default=4)
+    p.add_argument("--pmc-probe", action="store_true",
+                   help="run a 1 GiB copy and one call of each entry point, then exit "
+                        "(for rocprofv3 counter passes)")
     return p.parse_args()
+
+
+def gemm_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes (fetch + write) of one clip GEMM launch, from the counter file,
+    or None when it is missing, for another workload or for other sources."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = dict(line.split(None, 1) for line in fh if line.strip() and not line.startswith("#"))
+    except OSError:
+        return None
+    rec = {k: v.strip() for k, v in rec.items()}
+    if rec.get("workload") != workload or rec.get("source_sha256") != gemm_source_sha():
+        return None
+    return float(rec["fetch_bytes"]) + float(rec["write_bytes"])
 
 
 def algorithmic_work(W, mode_forms):
@@ -145,6 +178,22 @@ def main():
     scale = 1.0 / W.B
     torch.cuda.synchronize()
 
+    if args.pmc_probe:
+        # Calibration copy of known size, then one launch of each entry point.
+        x = torch.empty(2 ** 28, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)
+        torch.cuda.synchronize()
+        dpsgd.dpsgd_per_example_norms_multi(Ls, dpsgd.DPSGD_NORM_AUTO, buf.norms_sq,
+                                            workspace=buf.norms_ws)
+        dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, workspace=buf.clip_ws)
+        dpsgd.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_probe": W.name, "copy_bytes_each_way": x.numel() * 4,
+                          "gemm_source_sha256": gemm_source_sha()}), flush=True)
+        return
+
     def step(ev=None):
         if ev is not None:
             ev[0].record()
@@ -180,6 +229,7 @@ def main():
     mfma_peak = PEAK_BF16_TFLOPS if W.dtype == "bf16" else PEAK_FP32_TFLOPS
     clip_tflops = work["clip_flops"] / (t_clip * 1e-3) / 1e12
     norm_tflops = work["norm_flops"] / (t_norm * 1e-3) / 1e12
+    norm_gbs = work["input_bytes"] / (t_norm * 1e-3) / 1e9
     noise_gbs = work["noise_bytes"] / (t_noise * 1e-3) / 1e9
     value = W.B / (ms_per_step * 1e-3)
 
@@ -205,16 +255,19 @@ def main():
         "examples_per_s_per_layer": value * W.n_layers,
         "roofline": {
             "bound": "mfma",
-            "kernel": "clip-weighted sum (tgemm_kernel)",
+            "kernel": (f"clip-weighted sum {DOMINANT}, timed as the whole "
+                       "dpsgd_clip_accumulate_multi call (also clip_factors_kernel and "
+                       "tr_fixup_kernel)"),
             "achieved": clip_tflops,
             "peak": mfma_peak,
             "unit": "TFLOP/s",
             "frac": clip_tflops / mfma_peak,
-            "traffic": None,
+            "traffic": measured_traffic(W.name),
         },
         "kernels": {
             "norms_ms": t_norm, "norms_tflops": norm_tflops,
             "norms_frac_mfma": norm_tflops / mfma_peak,
+            "norms_input_gbs": norm_gbs, "norms_frac_hbm": norm_gbs / PEAK_HBM_GBS,
             "clip_ms": t_clip, "clip_tflops": clip_tflops,
             "noise_ms": t_noise, "noise_gbs": noise_gbs, "noise_frac_hbm": noise_gbs / PEAK_HBM_GBS,
             "norm_forms": {f: forms.count(f) for f in set(forms)},
