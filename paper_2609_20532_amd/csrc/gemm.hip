@@ -234,14 +234,19 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_kernel(TGemmArgs args) {
   auto fetch = [&](int64_t q) {
     const StepRows sr = step_rows<BK, PER_EXAMPLE>(q, T, B);
     int nrows_eff = sr.nrows;
-    if (SCALE == SCALE_ACC && g_side && args.factors[sr.ex] == 0.0f) nrows_eff = 0;
+    // Rows of an example whose factor is 0 are read as zeros on both sides, so
+    // that example contributes exactly nothing, also when its inputs are not
+    // finite.
+    if (SCALE == SCALE_ACC && args.factors[sr.ex] == 0.0f) nrows_eff = 0;
     tload<TIn, VEC>(X, R, col0, sr, nrows_eff, rbuf);
     if (SCALE == SCALE_OPERAND) {
       const int kb = (tid & 127) % TBlock<TIn>::KB;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int64_t row = sr.row0 + kb * 8 + j;
-        wrow[j] = (g_side && kb * 8 + j < sr.nrows) ? args.factors[row / T] : 1.0f;
+        const float c = kb * 8 + j < sr.nrows ? args.factors[row / T] : 1.0f;
+        wrow[j] = g_side ? c : 1.0f;
+        if (c == 0.0f) rbuf[j] = make_uint4(0u, 0u, 0u, 0u);
       }
     }
   };

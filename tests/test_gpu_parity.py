@@ -287,6 +287,42 @@ def test_zero_factor_examples_contribute_nothing(dp, shape):
     assert_sum_close(torch_to_float64(grad), ref, TOL[dtype], "clipped sum with zero factors")
 
 
+@pytest.mark.parametrize("shape", [CLIP_SHAPES[1], CLIP_SHAPES[2], CLIP_SHAPES[4], CLIP_SHAPES[-2]])
+def test_zero_factor_example_with_nonfinite_inputs_contributes_nothing(dp, shape):
+    """Reading: an example whose factor is 0 adds nothing to the sum, even when
+    its activations and gradients hold inf or NaN (its rows are not used)."""
+    import torch
+    B, T, d_in, d_out, dtype = shape
+    h = _host_layer(B, T, d_in, d_out, dtype, seed=B * 13 + T, g_scale=0.05)
+    ol = oracle_layers([h])
+    nsq_ref = oracle.per_example_norms_sq(ol).astype(np.float32)
+    bad = 1
+    nsq_ref[bad] = np.inf
+    A_bad = h.A.copy()
+    G_bad = h.G.copy()
+    inf_bits = wl.bf16_bits_from_f32(np.array([np.inf], np.float32))[0] if dtype == wl.BF16 else np.inf
+    nan_bits = wl.bf16_bits_from_f32(np.array([np.nan], np.float32))[0] if dtype == wl.BF16 else np.nan
+    A_bad[bad].flat[::7] = inf_bits
+    G_bad[bad].flat[::5] = nan_bits
+    hb = wl.HostLayer(A=A_bad, G=G_bad, d_in=d_in, d_out=d_out, tensor_id=h.tensor_id,
+                      dtype=dtype)
+    (L, A, G), = device_layers([hb])
+    C = float(np.median(np.sqrt(nsq_ref[np.isfinite(nsq_ref)])))
+    nsq = torch.from_numpy(nsq_ref).cuda()
+    grad = torch.zeros((d_out, d_in), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(dp.dpsgd_clip_workspace_bytes(L), 1), dtype=torch.uint8, device="cuda")
+    dp.dpsgd_clip_accumulate(L, nsq, C, grad, workspace=ws)
+    _sync()
+    _, c_ref, _ = oracle.clip_factors(nsq_ref.astype(np.float64), C)
+    assert c_ref[bad] == 0.0
+    keep = np.arange(B) != bad
+    ref = oracle.clipped_sum(oracle.OracleLayer(ol[0].A[keep], ol[0].G[keep], ol[0].tensor_id),
+                             c_ref[keep])
+    got = torch_to_float64(grad)
+    assert np.all(np.isfinite(got))
+    assert_sum_close(got, ref, TOL[dtype], "clipped sum without the zero-factor example")
+
+
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2], CLIP_SHAPES[-1]])
 def test_clip_sum_accumulates(dp, shape):
     h, got, ref, *_ = _clip_case(dp, shape, 1.0, accumulate=True)
