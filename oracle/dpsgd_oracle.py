@@ -214,3 +214,51 @@ def sampled_clipped_sum(layer: OracleLayer, factors: np.ndarray,
             acc += float(factors[i]) * float(layer.G[i, :, m] @ layer.A[i, :, nn])
         out[k] = acc
     return out
+
+
+# --------------------------------------------------------------- optimizer step
+
+
+@dataclass
+class AdamWConfig:
+    """AdamW hyper-parameters of one optimizer step (appendix "One-step AdamW
+    map"): learning rate eta_t, (beta1, beta2), epsilon, decoupled weight decay
+    lambda, and the step index t >= 1 of the bias corrections."""
+
+    lr: float
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    weight_decay: float = 0.0
+    t: int = 1
+
+
+def adamw_step(theta: np.ndarray, m: np.ndarray, v: np.ndarray, g: np.ndarray,
+               cfg: AdamWConfig) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """One AdamW step in float64: returns (theta_next, m_next, v_next).
+
+    The appendix's one-step map, written out: m = beta1 m + (1 - beta1) g;
+    v = beta2 v + (1 - beta2) g*g; m_hat = m / (1 - beta1^t); v_hat = v /
+    (1 - beta2^t); theta_next = theta - eta (m_hat / (sqrt(v_hat) + eps) +
+    lambda theta). The GPU algorithm applies it (its OptStep) to the noisy
+    averaged gradient.
+    """
+    theta = np.asarray(theta, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    m_new = cfg.beta1 * np.asarray(m, dtype=np.float64) + (1.0 - cfg.beta1) * g
+    v_new = cfg.beta2 * np.asarray(v, dtype=np.float64) + (1.0 - cfg.beta2) * g * g
+    m_hat = m_new / (1.0 - cfg.beta1 ** cfg.t)
+    v_hat = v_new / (1.0 - cfg.beta2 ** cfg.t)
+    theta_new = theta - cfg.lr * (m_hat / (np.sqrt(v_hat) + cfg.eps) + cfg.weight_decay * theta)
+    return theta_new, m_new, v_new
+
+
+def noise_adamw(S: np.ndarray, theta: np.ndarray, m: np.ndarray, v: np.ndarray, sigma: float,
+                C: float, seed: int, tensor_id: int, step: int, scale: float,
+                cfg: AdamWConfig):
+    """The GPU algorithm's last two steps for one layer: the noisy averaged
+    gradient g_tilde = scale * (S + sigma*C*z) (:func:`add_noise`), then the
+    optimizer step on it. Returns (g_tilde, theta_next, m_next, v_next)."""
+    g_tilde = add_noise(S, sigma, C, seed, tensor_id, step, scale)
+    theta_new, m_new, v_new = adamw_step(theta, m, v, g_tilde, cfg)
+    return g_tilde, theta_new, m_new, v_new

@@ -21,6 +21,7 @@ from oracle import (OracleLayer, add_noise, clip_factors, clipped_sum, dpsgd_ste
                     ghost_norm_sq_loops, per_example_gradient, per_example_norms_sq,
                     sampled_clipped_sum)
 from oracle import philox
+import oracle
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -351,3 +352,83 @@ def test_uniforms_are_exact_and_in_range():
     u_a, v_a, u_b, v_b = philox.uniforms(words)
     assert u_a[0] == 2.0 ** -24 and v_a[0] == 0.0
     assert u_b[0] == 1.0 and v_b[0] == 1.0 - 2.0 ** -24
+
+
+# ------------------------------------------------------------- AdamW step
+
+
+def _torch_adamw_reference(theta, m, v, g, cfg):
+    """One step of torch.optim.AdamW (float64, CPU) from the given state."""
+    import torch
+    p = torch.nn.Parameter(torch.from_numpy(theta.copy()))
+    opt = torch.optim.AdamW([p], lr=cfg.lr, betas=(cfg.beta1, cfg.beta2), eps=cfg.eps,
+                            weight_decay=cfg.weight_decay, foreach=False)
+    opt.state[p] = {"step": torch.tensor(float(cfg.t - 1), dtype=torch.float64),
+                    "exp_avg": torch.from_numpy(m.copy()),
+                    "exp_avg_sq": torch.from_numpy(v.copy())}
+    p.grad = torch.from_numpy(g.copy())
+    opt.step()
+    st = opt.state[p]
+    return p.detach().numpy(), st["exp_avg"].numpy(), st["exp_avg_sq"].numpy()
+
+
+@pytest.mark.parametrize("t,wd", [(1, 0.0), (1, 1e-2), (7, 1e-2), (500, 0.1)])
+def test_adamw_step_matches_torch_adamw(t, wd):
+    """The appendix's one-step AdamW map equals torch.optim.AdamW's update."""
+    rng = np.random.default_rng(17 + t)
+    theta = rng.standard_normal(257)
+    m = rng.standard_normal(257) * 1e-3 if t > 1 else np.zeros(257)
+    v = np.abs(rng.standard_normal(257)) * 1e-6 if t > 1 else np.zeros(257)
+    g = rng.standard_normal(257) * 1e-2
+    cfg = oracle.AdamWConfig(lr=4e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=wd, t=t)
+    th, mm, vv = oracle.adamw_step(theta, m, v, g, cfg)
+    th_ref, m_ref, v_ref = _torch_adamw_reference(theta, m, v, g, cfg)
+    # Equal up to the order of float64 roundings (a few ulp).
+    np.testing.assert_allclose(mm, m_ref, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(vv, v_ref, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(th, th_ref, rtol=0, atol=1e-15)
+
+
+def test_adamw_first_step_closed_form():
+    """From zero moments at t = 1: m_hat = g and v_hat = g^2, so the update is
+    g / (|g| + eps); with lambda the parameter also shrinks by eta*lambda*theta."""
+    g = np.array([0.5, -2.0, 1e-3, -7.0])
+    theta = np.array([1.0, -1.0, 0.25, 3.0])
+    cfg = oracle.AdamWConfig(lr=0.01, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1, t=1)
+    th, m, v = oracle.adamw_step(theta, np.zeros(4), np.zeros(4), g, cfg)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-15)
+    np.testing.assert_allclose(v, 0.001 * g * g, rtol=1e-14)
+    expect = theta - 0.01 * (g / (np.abs(g) + 1e-8) + 0.1 * theta)
+    np.testing.assert_allclose(th, expect, rtol=1e-14, atol=1e-16)
+
+
+def test_adamw_zero_gradient_still_moves_by_momentum_and_decay():
+    """With g = 0 the step is driven by the first moment and the weight decay
+    (the appendix notes the parameters move even for a zero gradient)."""
+    theta = np.array([2.0, -3.0])
+    m = np.array([1e-3, -2e-3])
+    v = np.array([4e-6, 9e-6])
+    cfg = oracle.AdamWConfig(lr=0.1, beta1=0.5, beta2=0.75, eps=0.0, weight_decay=0.2, t=2)
+    th, mm, vv = oracle.adamw_step(theta, m, v, np.zeros(2), cfg)
+    np.testing.assert_allclose(mm, 0.5 * m)
+    np.testing.assert_allclose(vv, 0.75 * v)
+    m_hat = 0.5 * m / (1 - 0.5 ** 2)
+    v_hat = 0.75 * v / (1 - 0.75 ** 2)
+    np.testing.assert_allclose(th, theta - 0.1 * (m_hat / np.sqrt(v_hat) + 0.2 * theta), rtol=1e-15)
+
+
+def test_noise_adamw_is_noise_then_adamw():
+    """noise_adamw composes add_noise (sigma = 0: exactly scale * S) with the step."""
+    rng = np.random.default_rng(5)
+    S = rng.standard_normal((3, 5))
+    theta = rng.standard_normal((3, 5))
+    cfg = oracle.AdamWConfig(lr=1e-3, t=3, weight_decay=0.01)
+    m = rng.standard_normal((3, 5)) * 1e-2
+    v = np.abs(rng.standard_normal((3, 5))) * 1e-4
+    g0, th0, m0, v0 = oracle.noise_adamw(S, theta, m, v, 0.0, 1.0, 9, 2, 0, 0.25, cfg)
+    assert np.array_equal(g0, 0.25 * S)
+    th_ref, m_ref, v_ref = oracle.adamw_step(theta, m, v, 0.25 * S, cfg)
+    assert np.array_equal(th0, th_ref) and np.array_equal(m0, m_ref) and np.array_equal(v0, v_ref)
+    g1, *_ = oracle.noise_adamw(S, theta, m, v, 1.5, 2.0, 9, 2, 0, 0.25, cfg)
+    z = oracle.noise(S.size, 9, 2, 0).reshape(S.shape)
+    np.testing.assert_allclose(g1, 0.25 * (S + 3.0 * z), rtol=1e-15)
