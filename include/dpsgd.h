@@ -168,6 +168,48 @@ int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* co
                           void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Noise + AdamW step.  Paper: GPU-side algorithm, its last two steps (the
+ * noisy average g_tilde = g_bar + Noise(s; sigma C)/B, then OptStep on it);
+ * the update is the appendix's one-step AdamW map.
+ *
+ *   g          = scale * (grad[e] + sigma * C * z_e)       (z_e exactly as dpsgd_add_noise)
+ *   m[e]      <- beta1 * m[e] + (1 - beta1) * g
+ *   v[e]      <- beta2 * v[e] + (1 - beta2) * g * g
+ *   param[e]  <- param[e] - lr * ( (m[e] / (1 - beta1^t)) / (sqrt(v[e] / (1 - beta2^t)) + eps)
+ *                                  + weight_decay * param[e] )
+ *   noisy_out[e] = g                                       (only when noisy_out is not NULL)
+ *
+ * for e in [0, d_out*d_in), in float32 (the bias corrections are formed in
+ * double on the host). grad is read only. param, exp_avg (m), exp_avg_sq (v),
+ * grad and noisy_out are float32 [d_out][d_in] device buffers, 16-byte
+ * aligned, pairwise non-overlapping. The _multi form takes one pointer per
+ * layer in each array; noisy_outs may be NULL (no layer writes g) or hold
+ * NULL entries. The layer descriptor is read as in dpsgd_add_noise.
+ * Errors (DPSGD_ERR_INVALID_ARG): a NULL or misaligned required pointer, the
+ * noise arguments as in dpsgd_add_noise, lr < 0 or not finite, beta1 or beta2
+ * outside [0, 1), eps <= 0 or not finite, weight_decay < 0 or not finite,
+ * t == 0.
+ * ------------------------------------------------------------------------- */
+typedef struct dpsgd_adamw {
+  float lr;            /* learning rate eta_t of this step        */
+  float beta1;         /* first-moment decay, in [0, 1)           */
+  float beta2;         /* second-moment decay, in [0, 1)          */
+  float eps;           /* added to sqrt(v_hat), > 0               */
+  float weight_decay;  /* decoupled decay lambda, >= 0            */
+  uint32_t t;          /* optimizer step, >= 1 (bias corrections) */
+} dpsgd_adamw;
+
+int dpsgd_noise_adamw(const dpsgd_layer* layer, const float* grad, float* param, float* exp_avg,
+                      float* exp_avg_sq, float* noisy_out, float sigma, float C, uint64_t seed,
+                      uint32_t step, float scale, const dpsgd_adamw* opt, void* stream);
+
+int dpsgd_noise_adamw_multi(const dpsgd_layer* layers, int32_t n_layers,
+                            const float* const* grads, float* const* params,
+                            float* const* exp_avgs, float* const* exp_avg_sqs,
+                            float* const* noisy_outs, float sigma, float C, uint64_t seed,
+                            uint32_t step, float scale, const dpsgd_adamw* opt, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Inspection hooks for tests (same stream as dpsgd_add_noise).
  *   dpsgd_philox_u32: out[4*b + w] = word w of block (first_block + b), b < n_blocks.
  *   dpsgd_gaussian:   out[e] = z_e of the stream above for e < n.

@@ -207,6 +207,46 @@ int dpsgd_add_noise(const dpsgd_layer* layer, float* grad, float sigma, float C,
   return dpsgd_add_noise_multi(layer, 1, grads, sigma, C, seed, step, scale, stream);
 }
 
+int dpsgd_noise_adamw_multi(const dpsgd_layer* layers, int32_t n_layers,
+                            const float* const* grads, float* const* params,
+                            float* const* exp_avgs, float* const* exp_avg_sqs,
+                            float* const* noisy_outs, float sigma, float C, uint64_t seed,
+                            uint32_t step, float scale, const dpsgd_adamw* opt, void* stream) {
+  int st = check_layers(layers, n_layers, false);
+  if (st != DPSGD_OK) return st;
+  if (!grads || !params || !exp_avgs || !exp_avg_sqs || !opt) return DPSGD_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const void* need[4] = {grads[l], params[l], exp_avgs[l], exp_avg_sqs[l]};
+    for (const void* p : need)
+      if (!p || !aligned16(p)) return DPSGD_ERR_INVALID_ARG;
+    if (noisy_outs && noisy_outs[l] && !aligned16(noisy_outs[l])) return DPSGD_ERR_INVALID_ARG;
+  }
+  if (bad_float(sigma) || sigma < 0.0f || isinf(sigma)) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(C) || !(C > 0.0f) || isinf(C)) return DPSGD_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return DPSGD_ERR_INVALID_ARG;
+  const dpsgd_adamw& o = *opt;
+  if (!isfinite(o.lr) || o.lr < 0.0f) return DPSGD_ERR_INVALID_ARG;
+  if (!(o.beta1 >= 0.0f && o.beta1 < 1.0f) || !(o.beta2 >= 0.0f && o.beta2 < 1.0f))
+    return DPSGD_ERR_INVALID_ARG;
+  if (!isfinite(o.eps) || !(o.eps > 0.0f)) return DPSGD_ERR_INVALID_ARG;
+  if (!isfinite(o.weight_decay) || o.weight_decay < 0.0f) return DPSGD_ERR_INVALID_ARG;
+  if (o.t == 0) return DPSGD_ERR_INVALID_ARG;
+  return launch_noise_adamw(layers, n_layers, grads, params, exp_avgs, exp_avg_sqs, noisy_outs,
+                            sigma, C, seed, step, scale, o, static_cast<hipStream_t>(stream));
+}
+
+int dpsgd_noise_adamw(const dpsgd_layer* layer, const float* grad, float* param, float* exp_avg,
+                      float* exp_avg_sq, float* noisy_out, float sigma, float C, uint64_t seed,
+                      uint32_t step, float scale, const dpsgd_adamw* opt, void* stream) {
+  const float* grads[1] = {grad};
+  float* params[1] = {param};
+  float* ms[1] = {exp_avg};
+  float* vs[1] = {exp_avg_sq};
+  float* outs[1] = {noisy_out};
+  return dpsgd_noise_adamw_multi(layer, 1, grads, params, ms, vs, outs, sigma, C, seed, step,
+                                 scale, opt, stream);
+}
+
 int dpsgd_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
                      uint32_t tensor_id, uint32_t step, void* stream) {
   if (!out || first_block < 0 || n_blocks < 0) return DPSGD_ERR_INVALID_ARG;

@@ -121,6 +121,10 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
 int launch_noise(const dpsgd_layer* layers, int n_layers, float* const* grads, float sigma,
                  float C, uint64_t seed, uint32_t step, float scale, hipStream_t stream);
 
+int launch_noise_adamw(const dpsgd_layer* layers, int n_layers, const float* const* grads,
+                       float* const* params, float* const* ms, float* const* vs,
+                       float* const* noisy, float sigma, float C, uint64_t seed, uint32_t step,
+                       float scale, const dpsgd_adamw& opt, hipStream_t stream);
 int launch_philox_u32(uint32_t* out, int64_t first_block, int64_t n_blocks, uint64_t seed,
                       uint32_t tensor_id, uint32_t step, hipStream_t stream);
 int launch_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, uint32_t step,

@@ -10,6 +10,8 @@
 // rounds, two 32x32->64 products each) and two log/sqrt/sin/cos sets per four
 // elements. Each thread owns whole 16-byte blocks so loads and stores are
 // 16-byte, fully coalesced, and every launch covers all tensors of the call.
+#include <math.h>
+
 #include "common.h"
 
 namespace dpsgd {
@@ -142,6 +144,91 @@ __global__ __launch_bounds__(kThreads) void gaussian_kernel(float* out, int64_t 
     if (e0 + w < n) out[e0 + w] = zz[w];
 }
 
+// ------------------------------------------------------- noise + AdamW step
+
+struct AdamSeg {
+  const float* grad;   // clipped sum S (read only)
+  float* param;
+  float* m;
+  float* v;
+  float* noisy;        // optional output of the noisy gradient (nullptr: not written)
+  int64_t numel;
+  uint32_t tensor_id;
+  uint32_t wg_begin;
+};
+
+struct AdamArgs {
+  AdamSeg seg[kMaxLayersPerLaunch];
+  int n_seg;
+  uint32_t k0, k1, step;
+  float sigmaC, scale;
+  float beta1, beta2, one_m_beta1, one_m_beta2;
+  float step_size;      // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;   // 1 / sqrt(1 - beta2^t)
+  float eps;
+  float decay;          // 1 - lr * weight_decay
+};
+
+// One element of the update: g = scale (S + sigma C z); moments; decoupled
+// decay and the bias-corrected step (appendix "One-step AdamW map").
+__device__ __forceinline__ void adamw_elem(const AdamArgs& a, float S, float z, float& p, float& m,
+                                           float& v, float& g) {
+  g = a.scale * fmaf(a.sigmaC, z, S);
+  m = fmaf(a.beta1, m, a.one_m_beta1 * g);
+  v = fmaf(a.beta2, v, a.one_m_beta2 * (g * g));
+  const float denom = fmaf(sqrtf(v), a.inv_sqrt_bc2, a.eps);
+  p = fmaf(p, a.decay, -a.step_size * (m / denom));
+}
+
+__global__ __launch_bounds__(kThreads) void noise_adamw_kernel(AdamArgs args) {
+  int lo = 0, hi = args.n_seg - 1;
+  const uint32_t wg = blockIdx.x;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.seg[mid].wg_begin <= wg) lo = mid; else hi = mid - 1;
+  }
+  const AdamSeg& s = args.seg[lo];
+  const int64_t first_block = (int64_t)(wg - s.wg_begin) * kBlocksPerWG;
+  const int64_t n_blocks = (s.numel + 3) >> 2;
+  const bool with_noise = args.sigmaC != 0.0f;
+
+#pragma unroll
+  for (int u = 0; u < kBlocksPerThread; ++u) {
+    const int64_t j = first_block + (int64_t)u * kThreads + threadIdx.x;
+    if (j >= n_blocks) break;
+    float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (with_noise) z = normals_of_block((uint64_t)j, s.tensor_id, args.step, args.k0, args.k1);
+    const int64_t e0 = j * 4;
+    if (e0 + 4 <= s.numel) {   // every pointer is 16-byte aligned (checked by the API)
+      const float4 S = *reinterpret_cast<const float4*>(s.grad + e0);
+      float4 p = *reinterpret_cast<const float4*>(s.param + e0);
+      float4 m = *reinterpret_cast<const float4*>(s.m + e0);
+      float4 v = *reinterpret_cast<const float4*>(s.v + e0);
+      float4 g;
+      adamw_elem(args, S.x, z.x, p.x, m.x, v.x, g.x);
+      adamw_elem(args, S.y, z.y, p.y, m.y, v.y, g.y);
+      adamw_elem(args, S.z, z.z, p.z, m.z, v.z, g.z);
+      adamw_elem(args, S.w, z.w, p.w, m.w, v.w, g.w);
+      *reinterpret_cast<float4*>(s.param + e0) = p;
+      *reinterpret_cast<float4*>(s.m + e0) = m;
+      *reinterpret_cast<float4*>(s.v + e0) = v;
+      if (s.noisy) *reinterpret_cast<float4*>(s.noisy + e0) = g;
+    } else {
+      const float zz[4] = {z.x, z.y, z.z, z.w};
+      for (int w = 0; w < 4; ++w) {
+        const int64_t e = e0 + w;
+        if (e >= s.numel) break;
+        float p = s.param[e], m = s.m[e], v = s.v[e], g;
+        adamw_elem(args, s.grad[e], zz[w], p, m, v, g);
+        s.param[e] = p;
+        s.m[e] = m;
+        s.v[e] = v;
+        if (s.noisy) s.noisy[e] = g;
+      }
+    }
+  }
+}
+
 }  // namespace
 
 int launch_noise(const dpsgd_layer* layers, int n_layers, float* const* grads, float sigma,
@@ -190,6 +277,51 @@ int launch_gaussian(float* out, int64_t n, uint64_t seed, uint32_t tensor_id, ui
   hipLaunchKernelGGL(gaussian_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, out, n,
                      (uint32_t)seed, (uint32_t)(seed >> 32), tensor_id, step);
   return check_launch();
+}
+
+int launch_noise_adamw(const dpsgd_layer* layers, int n_layers, const float* const* grads,
+                       float* const* params, float* const* ms, float* const* vs,
+                       float* const* noisy, float sigma, float C, uint64_t seed, uint32_t step,
+                       float scale, const dpsgd_adamw& opt, hipStream_t stream) {
+  const double bc1 = 1.0 - pow((double)opt.beta1, (double)opt.t);
+  const double bc2 = 1.0 - pow((double)opt.beta2, (double)opt.t);
+  for (int base = 0; base < n_layers; base += kMaxLayersPerLaunch) {
+    const int n = n_layers - base < kMaxLayersPerLaunch ? n_layers - base : kMaxLayersPerLaunch;
+    AdamArgs args{};
+    args.n_seg = n;
+    args.k0 = (uint32_t)seed;
+    args.k1 = (uint32_t)(seed >> 32);
+    args.step = step;
+    args.sigmaC = sigma * C;
+    args.scale = scale;
+    args.beta1 = opt.beta1;
+    args.beta2 = opt.beta2;
+    args.one_m_beta1 = (float)(1.0 - (double)opt.beta1);
+    args.one_m_beta2 = (float)(1.0 - (double)opt.beta2);
+    args.step_size = (float)((double)opt.lr / bc1);
+    args.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+    args.eps = opt.eps;
+    args.decay = (float)(1.0 - (double)opt.lr * (double)opt.weight_decay);
+    int64_t wgs = 0;
+    for (int l = 0; l < n; ++l) {
+      const dpsgd_layer& L = layers[base + l];
+      AdamSeg& sg = args.seg[l];
+      sg.grad = grads[base + l];
+      sg.param = params[base + l];
+      sg.m = ms[base + l];
+      sg.v = vs[base + l];
+      sg.noisy = noisy ? noisy[base + l] : nullptr;
+      sg.numel = L.d_out * L.d_in;
+      sg.tensor_id = L.tensor_id;
+      sg.wg_begin = (uint32_t)wgs;
+      wgs += ceil_div(ceil_div(sg.numel, 4), kBlocksPerWG);
+    }
+    if (wgs <= 0) continue;
+    if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(noise_adamw_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, args);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
 }
 
 }  // namespace dpsgd

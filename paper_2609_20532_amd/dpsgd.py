@@ -34,8 +34,8 @@ EXPORTED = (
     "dpsgd_norms_workspace_bytes", "dpsgd_select_norm_mode", "dpsgd_per_example_norms",
     "dpsgd_per_example_norms_multi", "dpsgd_clip_factors", "dpsgd_clip_workspace_bytes",
     "dpsgd_clip_accumulate", "dpsgd_clip_accumulate_multi", "dpsgd_add_noise",
-    "dpsgd_add_noise_multi", "dpsgd_philox_u32", "dpsgd_gaussian", "dpsgd_status_string",
-    "dpsgd_version",
+    "dpsgd_add_noise_multi", "dpsgd_noise_adamw", "dpsgd_noise_adamw_multi",
+    "dpsgd_philox_u32", "dpsgd_gaussian", "dpsgd_status_string", "dpsgd_version",
 )
 
 
@@ -55,6 +55,17 @@ class dpsgd_layer(ctypes.Structure):  # noqa: N801 - mirrors the C struct name
         ("d_out", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
         ("tensor_id", ctypes.c_uint32),
+    ]
+
+
+class dpsgd_adamw(ctypes.Structure):  # noqa: N801 - mirrors the C struct name
+    _fields_ = [
+        ("lr", ctypes.c_float),
+        ("beta1", ctypes.c_float),
+        ("beta2", ctypes.c_float),
+        ("eps", ctypes.c_float),
+        ("weight_decay", ctypes.c_float),
+        ("t", ctypes.c_uint32),
     ]
 
 
@@ -79,6 +90,10 @@ def _declare(lib):
                                         [L, i32, vp, f32, P(vp), i32, vp, vp, vp, sz, vp]),
         "dpsgd_add_noise": (ctypes.c_int, [L, vp, f32, f32, u64, u32, f32, vp]),
         "dpsgd_add_noise_multi": (ctypes.c_int, [L, i32, P(vp), f32, f32, u64, u32, f32, vp]),
+        "dpsgd_noise_adamw": (ctypes.c_int, [L, vp, vp, vp, vp, vp, f32, f32, u64, u32, f32,
+                                             P(dpsgd_adamw), vp]),
+        "dpsgd_noise_adamw_multi": (ctypes.c_int, [L, i32, P(vp), P(vp), P(vp), P(vp), P(vp),
+                                                   f32, f32, u64, u32, f32, P(dpsgd_adamw), vp]),
         "dpsgd_philox_u32": (ctypes.c_int, [vp, i64, i64, u64, u32, u32, vp]),
         "dpsgd_gaussian": (ctypes.c_int, [vp, i64, u64, u32, u32, vp]),
         "dpsgd_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -157,7 +172,7 @@ def _array(layers):
 
 
 def _ptr_array(tensors):
-    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+    return (ctypes.c_void_p * len(tensors))(*[None if t is None else t.data_ptr() for t in tensors])
 
 
 # ------------------------------------------------------------- entry points
@@ -246,6 +261,31 @@ def dpsgd_add_noise_multi(layers, grads, sigma, C, seed, step, scale, stream=Non
     st = _lib.dpsgd_add_noise_multi(arr, n, _ptr_array(grads), sigma, C, seed, step, scale,
                                     _stream(stream))
     _check("dpsgd_add_noise_multi", st)
+
+
+def make_adamw(lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, t=1) -> dpsgd_adamw:
+    return dpsgd_adamw(lr=lr, beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay, t=t)
+
+
+def dpsgd_noise_adamw(layer, grad, param, exp_avg, exp_avg_sq, sigma, C, seed, step, scale, opt,
+                      noisy_out=None, stream=None):
+    load()
+    st = _lib.dpsgd_noise_adamw(ctypes.byref(layer), _ptr(grad), _ptr(param), _ptr(exp_avg),
+                                _ptr(exp_avg_sq), _ptr(noisy_out), sigma, C, seed, step, scale,
+                                ctypes.byref(opt), _stream(stream))
+    _check("dpsgd_noise_adamw", st)
+
+
+def dpsgd_noise_adamw_multi(layers, grads, params, exp_avgs, exp_avg_sqs, sigma, C, seed, step,
+                            scale, opt, noisy_outs=None, stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_noise_adamw_multi(arr, n, _ptr_array(grads), _ptr_array(params),
+                                      _ptr_array(exp_avgs), _ptr_array(exp_avg_sqs),
+                                      None if noisy_outs is None else _ptr_array(noisy_outs),
+                                      sigma, C, seed, step, scale, ctypes.byref(opt),
+                                      _stream(stream))
+    _check("dpsgd_noise_adamw_multi", st)
 
 
 def dpsgd_philox_u32(out, first_block, n_blocks, seed, tensor_id, step, stream=None):

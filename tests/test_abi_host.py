@@ -138,3 +138,42 @@ def test_hooks_reject_bad_args_and_accept_empty(lib):
     assert lib.dpsgd_philox_u32(ctypes.c_void_p(64), 0, 0, 1, 0, 0, None) == 0
     assert lib.dpsgd_gaussian(ctypes.c_void_p(64), -5, 1, 0, 0, None) == -1
     assert lib.dpsgd_gaussian(ctypes.c_void_p(64), 0, 1, 0, 0, None) == 0
+
+
+def test_adamw_struct_layout():
+    assert ctypes.sizeof(dpsgd.dpsgd_adamw) == 24
+    assert dpsgd.dpsgd_adamw.t.offset == 20
+
+
+_GOOD_ADAMW = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, t=1)
+
+
+@pytest.mark.parametrize("bad", [dict(lr=-1.0), dict(lr=float("inf")), dict(beta1=1.0),
+                                 dict(beta1=-0.1), dict(beta2=1.0), dict(beta2=float("nan")),
+                                 dict(eps=0.0), dict(eps=float("inf")), dict(weight_decay=-1e-3),
+                                 dict(weight_decay=float("nan")), dict(t=0)])
+def test_noise_adamw_rejects_bad_hyperparameters(lib, bad):
+    L = _lay()
+    opt = dpsgd.make_adamw(**{**_GOOD_ADAMW, **bad})
+    p = [ctypes.c_void_p(256 * (k + 1)) for k in range(4)]
+    assert lib.dpsgd_noise_adamw(ctypes.byref(L), *p, None, 1.0, 1.0, 1, 0, 1.0,
+                                 ctypes.byref(opt), None) == -1
+
+
+def test_noise_adamw_rejects_null_and_misaligned_buffers(lib):
+    L = _lay()
+    opt = dpsgd.make_adamw(**_GOOD_ADAMW)
+    good = [ctypes.c_void_p(256 * (k + 1)) for k in range(4)]
+    for k in range(4):
+        for bad in (None, ctypes.c_void_p(256 * (k + 1) + 4)):
+            p = list(good)
+            p[k] = bad
+            assert lib.dpsgd_noise_adamw(ctypes.byref(L), *p, None, 1.0, 1.0, 1, 0, 1.0,
+                                         ctypes.byref(opt), None) == -1
+    # misaligned optional output, NULL optimizer config, bad noise scalars
+    assert lib.dpsgd_noise_adamw(ctypes.byref(L), *good, ctypes.c_void_p(2052), 1.0, 1.0, 1, 0,
+                                 1.0, ctypes.byref(opt), None) == -1
+    assert lib.dpsgd_noise_adamw(ctypes.byref(L), *good, None, 1.0, 1.0, 1, 0, 1.0, None,
+                                 None) == -1
+    assert lib.dpsgd_noise_adamw(ctypes.byref(L), *good, None, -1.0, 1.0, 1, 0, 1.0,
+                                 ctypes.byref(opt), None) == -1
