@@ -105,7 +105,7 @@ def algorithmic_work(W, mode_forms):
         noise_elems += s.d_in * s.d_out
     return dict(norm_flops=norm_flops, clip_flops=clip_flops, input_bytes=in_bytes,
                 clip_bytes=in_bytes + 4.0 * noise_elems, noise_bytes=8.0 * noise_elems,
-                noise_elems=noise_elems)
+                noise_adamw_bytes=28.0 * noise_elems, noise_elems=noise_elems)
 
 
 def cpu_baseline(W, dev_layers, n_examples: int):
@@ -149,6 +149,39 @@ def cpu_baseline(W, dev_layers, n_examples: int):
     }
 
 
+def time_noise_adamw(dpsgd, Ls, buf, W, scale, steps):
+    """Average duration of the fused noise + AdamW pass over every layer.
+
+    Timed on its own, after the step: the optimizer update is not part of the
+    gradient step whose throughput is reported.  Parameters and moments are
+    float32 buffers the size of each layer's weight; no noisy-gradient copy is
+    written (28 bytes of HBM traffic per parameter).
+    """
+    import torch
+    params = [torch.randn_like(g) for g in buf.grads]
+    ms = [torch.zeros_like(g) for g in buf.grads]
+    vs = [torch.zeros_like(g) for g in buf.grads]
+    opt = dpsgd.make_adamw(lr=1e-3, weight_decay=1e-2, t=1)
+
+    def run():
+        dpsgd.dpsgd_noise_adamw_multi(Ls, buf.grads, params, ms, vs, W.sigma, W.C,
+                                      W.noise_seed, W.step, scale, opt)
+
+    for _ in range(3):
+        run()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    t = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    del params, ms, vs
+    return t
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -189,6 +222,13 @@ def main():
                                             workspace=buf.norms_ws)
         dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, workspace=buf.clip_ws)
         dpsgd.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
+        params = [torch.randn_like(g) for g in buf.grads]
+        moms = [torch.zeros_like(g) for g in buf.grads]
+        moms2 = [torch.zeros_like(g) for g in buf.grads]
+        torch.cuda.synchronize()
+        dpsgd.dpsgd_noise_adamw_multi(Ls, buf.grads, params, moms, moms2, W.sigma, W.C,
+                                      W.noise_seed, W.step, scale,
+                                      dpsgd.make_adamw(lr=1e-3, weight_decay=1e-2))
         torch.cuda.synchronize()
         print(json.dumps({"pmc_probe": W.name, "copy_bytes_each_way": x.numel() * 4,
                           "gemm_source_sha256": gemm_source_sha()}), flush=True)
@@ -225,6 +265,9 @@ def main():
     t_norm = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     t_clip = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     t_noise = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+
+    t_adamw = time_noise_adamw(dpsgd, Ls, buf, W, scale, args.steps)
+    adamw_gbs = work["noise_adamw_bytes"] / (t_adamw * 1e-3) / 1e9
 
     mfma_peak = PEAK_BF16_TFLOPS if W.dtype == "bf16" else PEAK_FP32_TFLOPS
     clip_tflops = work["clip_flops"] / (t_clip * 1e-3) / 1e12
@@ -270,6 +313,8 @@ def main():
             "norms_input_gbs": norm_gbs, "norms_frac_hbm": norm_gbs / PEAK_HBM_GBS,
             "clip_ms": t_clip, "clip_tflops": clip_tflops,
             "noise_ms": t_noise, "noise_gbs": noise_gbs, "noise_frac_hbm": noise_gbs / PEAK_HBM_GBS,
+            "noise_adamw_ms": t_adamw, "noise_adamw_gbs": adamw_gbs,
+            "noise_adamw_frac_hbm": adamw_gbs / PEAK_HBM_GBS,
             "norm_forms": {f: forms.count(f) for f in set(forms)},
             "algorithmic": work,
         },
