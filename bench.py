@@ -39,8 +39,16 @@ METRIC = "DP-SGD clipped+noised grad throughput: examples/s per layer; % MFMA pe
 # only for the kernel sources they were taken with.
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "clip_gemm_c5_traffic.txt")
 GEMM_SOURCES = [os.path.join(HERE, "paper_2609_20532_amd", "csrc", f)
-                for f in ("gemm_tr.hip", "lds_dma.h", "mma.h", "common.h")]
-DOMINANT = "tgemm_tr_kernel<0>"
+                for f in ("gemm_wide.hip", "gemm_tr.hip", "gemm.hip", "lds_dma.h", "mma.h",
+                          "common.h")]
+
+
+def dominant_kernel(W) -> str:
+    """The clip kernel that carries the workload's bf16 layers: the 384x256-tile
+    kernel when every layer fits it, else the 256x256-tile kernel."""
+    wide = all(W.dtype == "bf16" and s.d_out % 384 == 0 and s.d_in % 256 == 0 and W.T % 32 == 0
+               for s in W.layers)
+    return "tgemm_wide_kernel" if wide else "tgemm_tr_kernel<0>"
 
 
 def parse():
@@ -298,9 +306,9 @@ def main():
         "examples_per_s_per_layer": value * W.n_layers,
         "roofline": {
             "bound": "mfma",
-            "kernel": (f"clip-weighted sum {DOMINANT}, timed as the whole "
+            "kernel": (f"clip-weighted sum {dominant_kernel(W)}, timed as the whole "
                        "dpsgd_clip_accumulate_multi call (also clip_factors_kernel and "
-                       "tr_fixup_kernel)"),
+                       "the split-K tail fix-up)"),
             "achieved": clip_tflops,
             "peak": mfma_peak,
             "unit": "TFLOP/s",

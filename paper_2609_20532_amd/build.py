@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdpsgd.so")
 OBJ_DIR = os.path.join(PKG, "_build")
-SOURCES = ["api.hip", "noise.hip", "norms.hip", "ghost.hip", "gemm.hip", "gemm_tr.hip"]
+SOURCES = ["api.hip", "noise.hip", "norms.hip", "ghost.hip", "gemm.hip", "gemm_tr.hip", "gemm_wide.hip"]
 ARCH = "gfx950"
 
 

@@ -94,6 +94,13 @@ void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrC
 int launch_tr_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
                    float* const* outs, int accumulate, const TrClipPlan& plan, float* tail_ws,
                    hipStream_t stream);
+// 384x256-tile clip kernel (gemm_wide.hip): bf16, d_out % 384 == 0,
+// d_in % 256 == 0, T % 32 == 0; preferred over the 256-tile kernel.
+bool wide_tile_ok(const dpsgd_layer& L);
+void plan_wide_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan);
+int launch_wide_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
+                     float* const* outs, int accumulate, const TrClipPlan& plan, float* tail_ws,
+                     hipStream_t stream);
 int launch_tr_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                         float* partials, int64_t P, hipStream_t stream);
 
@@ -111,6 +118,8 @@ struct ClipPlan {
   size_t partial_bytes;                          // total (split partials + 256-tile tail)
   TrClipPlan tr;                                 // layers on the 256-tile kernel
   size_t tr_offset;                              // their tail partials, from the partial base
+  TrClipPlan wide;                               // layers on the 384x256-tile kernel
+  size_t wide_offset;
 };
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan);
 

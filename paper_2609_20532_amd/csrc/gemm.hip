@@ -434,11 +434,12 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // then a split tail). The 128-tile layers are split along K only when they
   // have too few output tiles to occupy the GPU (two workgroups per CU).
   const int cus = tr_cu_count();
-  int tr_idx[kMaxLayersPerLaunch], n_tr = 0;
+  int tr_idx[kMaxLayersPerLaunch], n_tr = 0, wd_idx[kMaxLayersPerLaunch], n_wd = 0;
   int64_t tiles_small = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
-    if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
+    if (wide_tile_ok(L)) wd_idx[n_wd++] = l;
+    else if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
     else tiles_small += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
   }
   const int64_t target = 2 * (int64_t)cus;
@@ -460,8 +461,10 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
     if (s > 1) off += round_up((size_t)s * (size_t)L.d_out * (size_t)L.d_in * sizeof(float), 256);
   }
   plan_tr_clip(layers, tr_idx, n_tr, cus, &plan->tr);
+  plan_wide_clip(layers, wd_idx, n_wd, cus, &plan->wide);
   plan->tr_offset = off;
-  plan->partial_bytes = off + round_up(plan->tr.tail_bytes, 256);
+  plan->wide_offset = off + round_up(plan->tr.tail_bytes, 256);
+  plan->partial_bytes = plan->wide_offset + round_up(plan->wide.tail_bytes, 256);
 }
 
 int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factors,
@@ -469,15 +472,17 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
                     hipStream_t stream) {
   // Group layers by kernel variant; each group is one grouped launch.
   const bool bf16 = layers[0].dtype == DPSGD_BF16;
-  int idx[5][kMaxLayersPerLaunch];
-  float* outs[5][kMaxLayersPerLaunch];
-  int spl[5][kMaxLayersPerLaunch];
-  int acc[5][kMaxLayersPerLaunch];
-  int cnt[5] = {0, 0, 0, 0, 0};
+  int idx[6][kMaxLayersPerLaunch];
+  float* outs[6][kMaxLayersPerLaunch];
+  int spl[6][kMaxLayersPerLaunch];
+  int acc[6][kMaxLayersPerLaunch];
+  int cnt[6] = {0, 0, 0, 0, 0, 0};
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
-    const int g = tr_tile_ok(L) ? 4 : (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
+    const int g = wide_tile_ok(L) ? 5
+                  : tr_tile_ok(L) ? 4
+                                  : (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
     const int k = cnt[g]++;
     idx[g][k] = l;
     spl[g][k] = plan.splits[l];
@@ -493,6 +498,11 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
                         reinterpret_cast<float*>(reinterpret_cast<char*>(partial_base) +
                                                  plan.tr_offset),
                         stream);
+  if (st == DPSGD_OK && cnt[5])
+    st = launch_wide_clip(layers, idx[5], cnt[5], factors, outs[5], accumulate, plan.wide,
+                          reinterpret_cast<float*>(reinterpret_cast<char*>(partial_base) +
+                                                   plan.wide_offset),
+                          stream);
 #define DPSGD_TG(T_, V_, S_, g_)                                                                \
   if (st == DPSGD_OK && cnt[g_])                                                               \
   st = launch_tgemm_group<T_, V_, S_, EPI_STORE>(layers, idx[g_], cnt[g_], factors, outs[g_], \
