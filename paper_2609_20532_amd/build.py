@@ -1,9 +1,11 @@
-"""Build the gfx950 HIP library ``libdpsgd.so`` in-tree with hipcc.
+"""Build the gfx950 HIP library ``libdpsgd.so`` and the CPU verifier library
+``libdpsgd_verifier.so`` in-tree.
 
 Usage: ``python -m paper_2609_20532_amd.build`` (or ``build()`` from Python).
-Every source is compiled for gfx950 only. Packed fp32 instructions are switched
-off for the device code (``-packed-fp32-ops``): the compiler would otherwise
-fuse pairs of float operations into ``v_pk_*_f32`` forms.
+Every HIP source is compiled for gfx950 only. Packed fp32 instructions are
+switched off for the device code (``-packed-fp32-ops``): the compiler would
+otherwise fuse pairs of float operations into ``v_pk_*_f32`` forms. The
+verifier is plain host C++ (g++, x86-64-v3), with no GPU runtime.
 """
 
 from __future__ import annotations
@@ -19,6 +21,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdpsgd.so")
+VERIFIER_LIB = os.path.join(PKG, "libdpsgd_verifier.so")
+VERIFIER_SOURCES = ["verifier.cpp"]
 OBJ_DIR = os.path.join(PKG, "_build")
 SOURCES = ["api.hip", "noise.hip", "norms.hip", "ghost.hip", "gemm.hip", "gemm_tr.hip", "gemm_wide.hip"]
 ARCH = "gfx950"
@@ -53,11 +57,32 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
+def build_verifier(verbose: bool = False) -> str:
+    """Compile the host-only verifier into ``libdpsgd_verifier.so``."""
+    cxx = shutil.which("g++") or shutil.which("c++")
+    if not cxx:
+        raise RuntimeError("no C++ compiler found for the verifier library")
+    tmp = VERIFIER_LIB + ".tmp"
+    cmd = [cxx, "-O3", "-march=x86-64-v3", "-std=c++17", "-fPIC", "-shared", "-pthread",
+           "-Wall", "-Wextra", "-I", INCLUDE,
+           *[os.path.join(CSRC, s) for s in VERIFIER_SOURCES], "-o", tmp]
+    res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"verifier build failed:\n{res.stdout}")
+    if verbose and res.stdout.strip():
+        print(res.stdout)
+    os.replace(tmp, VERIFIER_LIB)
+    return VERIFIER_LIB
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source and link ``libdpsgd.so``; returns its path."""
+    """Compile every HIP source and link ``libdpsgd.so`` (and build the verifier
+    library); returns the path of ``libdpsgd.so``."""
     os.makedirs(OBJ_DIR, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES) + 1) as ex:
+        ver = ex.submit(build_verifier, verbose)
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        ver.result()
     tmp = LIB + ".tmp"
     cmd = [hipcc_path(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
