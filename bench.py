@@ -157,6 +157,33 @@ def cpu_baseline(W, dev_layers, n_examples: int):
     }
 
 
+def verifier_check(W, dev_layers, n_examples: int):
+    """Cost of the trusted side's float32 recomputation (the body-path check of
+    a sampled step) on this host's cores: the clipped average of every layer
+    for a few examples, scaled to the workload's B (the cost is linear in the
+    examples)."""
+    import torch
+    from paper_2609_20532_amd import verifier as V
+
+    b = min(n_examples, W.B)
+    hosts = []
+    for d in dev_layers:
+        A, G = d["A"][:b].cpu(), d["G"][:b].cpu()
+        if A.dtype == torch.bfloat16:
+            A, G = A.view(torch.int16).numpy().view(np.uint16), G.view(torch.int16).numpy().view(np.uint16)
+        else:
+            A, G = A.numpy(), G.numpy()
+        hosts.append(V.host_layer(A, G, d["tensor_id"]))
+    threads = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    V.dpsgd_reference_mean_f32(hosts, W.C, b, threads=threads)
+    t1 = time.perf_counter()
+    est = (t1 - t0) / b * W.B
+    return {"seconds_per_checked_step": est, "threads": threads,
+            "sample": (f"float32 recomputation of {b} of {W.B} examples x {len(hosts)} layers in "
+                       f"{t1 - t0:.2f} s, scaled to {W.B} examples")}
+
+
 def time_noise_adamw(dpsgd, Ls, buf, W, scale, steps):
     """Average duration of the fused noise + AdamW pass over every layer.
 
@@ -329,6 +356,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(W, layers_t, args.cpu_sample_examples)
+        out["verifier_check"] = verifier_check(W, layers_t, 2)
     print(json.dumps(out), flush=True)
 
 
