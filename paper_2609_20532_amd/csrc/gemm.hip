@@ -430,31 +430,38 @@ int launch_tgemm_group(const dpsgd_layer* layers, const int* idx, int n, const f
 }  // namespace
 
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
-  // Layers on the 256-tile kernel are balanced by its own plan (whole tiles,
-  // then a split tail). The 128-tile layers are split along K only when they
-  // have too few output tiles to occupy the GPU (two workgroups per CU).
+  // Layers on the 256- and 384x256-tile kernels are balanced by their own
+  // plans (whole tiles, then a split tail). The 128-tile layers split their K
+  // range so that every workgroup of the launch gets about the same number of
+  // K steps: the layers of one call can differ by orders of magnitude in
+  // B * T (a convolution's positions) and in output tiles, and a layer with
+  // few output tiles but a long K range would otherwise run on a handful of
+  // CUs.
   const int cus = tr_cu_count();
   int tr_idx[kMaxLayersPerLaunch], n_tr = 0, wd_idx[kMaxLayersPerLaunch], n_wd = 0;
-  int64_t tiles_small = 0;
+  int64_t work = 0;   // output tiles x K steps over the 128-tile layers
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     if (wide_tile_ok(L)) wd_idx[n_wd++] = l;
     else if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
-    else tiles_small += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+    else work += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile) *
+                 clip_q_total(L, clip_scale_mode(L));
   }
-  const int64_t target = 2 * (int64_t)cus;
-  const int64_t want_small =
-      tiles_small >= target ? 1 : ceil_div(target, tiles_small > 0 ? tiles_small : 1);
+  constexpr int64_t kMinStepsPerSplit = 4;
+  constexpr int64_t kMaxSplits = 1024;
+  const int64_t target = 4 * (int64_t)cus;   // workgroups
+  int64_t chunk = ceil_div(work > 0 ? work : 1, target);
+  if (chunk < kMinStepsPerSplit) chunk = kMinStepsPerSplit;
   size_t off = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     int64_t s = 1;
-    if (!tr_tile_ok(L)) {
+    if (!wide_tile_ok(L) && !tr_tile_ok(L)) {
       const int64_t q_total = clip_q_total(L, clip_scale_mode(L));
-      s = want_small;
-      if (s > q_total / 4) s = q_total / 4;  // at least 4 K steps per split
+      s = ceil_div(q_total, chunk);
+      if (s > q_total / kMinStepsPerSplit) s = q_total / kMinStepsPerSplit;
+      if (s > kMaxSplits) s = kMaxSplits;
       if (s < 1) s = 1;
-      if (s > 64) s = 64;
     }
     plan->splits[l] = (int)s;
     plan->partial_offset[l] = off;
