@@ -365,8 +365,7 @@ __global__ __launch_bounds__(kThreads) void split_reduce_kernel(SplitArgs args) 
 // ------------------------------------------------------------ host side
 
 int clip_scale_mode(const dpsgd_layer& L) {
-  if (L.dtype != DPSGD_BF16) return SCALE_OPERAND;
-  const int64_t bk = TileCfg<uint16_t>::BK;
+  const int64_t bk = L.dtype == DPSGD_BF16 ? TileCfg<uint16_t>::BK : TileCfg<float>::BK;
   const int64_t pad = ceil_div(L.T, bk) * bk - L.T;  // zero rows per example
   return pad * 8 <= L.T ? SCALE_ACC : SCALE_OPERAND;
 }
@@ -437,27 +436,35 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // B * T (a convolution's positions) and in output tiles, and a layer with
   // few output tiles but a long K range would otherwise run on a handful of
   // CUs.
+  // The balance is per launch: layers of different kernel instances (vector
+  // or element loads, weight on the accumulator or on the operand) run in
+  // separate launches, one after the other, so each launch fills the GPU on
+  // its own.
   const int cus = tr_cu_count();
   int tr_idx[kMaxLayersPerLaunch], n_tr = 0, wd_idx[kMaxLayersPerLaunch], n_wd = 0;
-  int64_t work = 0;   // output tiles x K steps over the 128-tile layers
+  int64_t work[4] = {0, 0, 0, 0};   // output tiles x K steps per 128-tile launch
+  auto group = [](const dpsgd_layer& L) {
+    const bool vec = L.dtype == DPSGD_BF16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
+    return (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
+  };
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     if (wide_tile_ok(L)) wd_idx[n_wd++] = l;
     else if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
-    else work += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile) *
-                 clip_q_total(L, clip_scale_mode(L));
+    else work[group(L)] += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile) *
+                           clip_q_total(L, clip_scale_mode(L));
   }
   constexpr int64_t kMinStepsPerSplit = 4;
   constexpr int64_t kMaxSplits = 1024;
-  const int64_t target = 4 * (int64_t)cus;   // workgroups
-  int64_t chunk = ceil_div(work > 0 ? work : 1, target);
-  if (chunk < kMinStepsPerSplit) chunk = kMinStepsPerSplit;
+  const int64_t target = 4 * (int64_t)cus;   // workgroups per launch
   size_t off = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     int64_t s = 1;
     if (!wide_tile_ok(L) && !tr_tile_ok(L)) {
       const int64_t q_total = clip_q_total(L, clip_scale_mode(L));
+      int64_t chunk = ceil_div(work[group(L)], target);
+      if (chunk < kMinStepsPerSplit) chunk = kMinStepsPerSplit;
       s = ceil_div(q_total, chunk);
       if (s > q_total / kMinStepsPerSplit) s = q_total / kMinStepsPerSplit;
       if (s > kMaxSplits) s = kMaxSplits;
@@ -520,6 +527,8 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
     DPSGD_TG(uint16_t, true, SCALE_OPERAND, 2);
     DPSGD_TG(uint16_t, false, SCALE_OPERAND, 3);
   } else {
+    DPSGD_TG(float, true, SCALE_ACC, 0);
+    DPSGD_TG(float, false, SCALE_ACC, 1);
     DPSGD_TG(float, true, SCALE_OPERAND, 2);
     DPSGD_TG(float, false, SCALE_OPERAND, 3);
   }

@@ -209,6 +209,8 @@ CLIP_SHAPES = [
     (12, 5, 64, 96, wl.BF16),       # small T: weight applied to the operand
     (4, 70, 13, 21, wl.BF16),       # non-vector loads
     (3, 9, 11, 7, wl.F32),
+    (4, 64, 96, 80, wl.F32),        # float32, T a multiple of the K step: weight on the accumulator
+    (3, 32, 27, 10, wl.F32),        # the same with element loads (widths not multiples of 4)
     (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
     (8, 256, 256, 256, wl.BF16),    # 256x256-tile kernel, split along K
     (4, 64, 256, 384, wl.BF16),     # 384x256-tile kernel, one tile split along K
