@@ -54,13 +54,18 @@ constexpr int kWdAGroup = 4 * kWdTN * 2;        // 2 KB: four A k-rows (8 units)
 constexpr int kWdGBytes = kWdBK / 4 * kWdGGroup;   // 24 KB
 constexpr int kWdABytes = kWdBK / 4 * kWdAGroup;   // 16 KB
 constexpr int kWdStageBytes = kWdGBytes + kWdABytes;
-constexpr int kWdStages = 4;
-constexpr int kWdLdsBytes = kWdStages * kWdStageBytes;   // 160 KB
+// Two ring slots: the next slice's copies run while the current one is
+// multiplied. Measured on the 48-layer step: 2 slots 5.63 ms, 3 slots 6.04,
+// 4 slots 5.78-5.83 (more bytes in flight do not help; 64-row slices in two
+// 80 KB slots, which halve the barriers, also gave 5.62-5.63).
+constexpr int kWdStages = 2;
+constexpr int kWdLdsBytes = kWdStages * kWdStageBytes;   // 80 KB
 constexpr int kWdGCopies = kWdGBytes / 1024;             // 24
 constexpr int kWdCopies = kWdStageBytes / 1024 / kWdWaves;  // 5 per wave per slice
 constexpr int kWdTileElems = kWdTM * kWdTN;
 static_assert(kWdGCopies % kWdWaves == 0, "G copies split evenly over the waves");
 static_assert(kWdLdsBytes <= 160 * 1024, "LDS budget");
+static_assert(kWdStages >= 2, "the ring needs a slot being filled and one being read");
 
 struct WdEntry {
   const void* G;          // [B*T][M]
@@ -234,7 +239,7 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
     const char* a0 = base + ra[0];
     const char* a1 = base + ra[1];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < kWdBK / 16; ++ks) {
       bf16x8_t b[kWdNB];
 #pragma unroll
       for (int j = 0; j < kWdNB; ++j) b[j] = wd_frag(a0, a1, ks * 4 * kWdAGroup + 256 * j);
