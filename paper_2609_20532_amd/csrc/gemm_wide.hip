@@ -4,20 +4,22 @@
 //   the example i = k / T (paper: Section 2.2, the clipped per-example
 //   gradients c_i g_i summed over the batch).
 //
-// Why a second tile shape: per FLOP, a 384 x 256 workgroup tile copies 17 %
-// fewer bytes into LDS than a 256 x 256 one, and a 96 x 128 wave sub-tile
-// (192 fp32 accumulators, two waves per SIMD) issues 22 % fewer transposed
-// LDS reads (ds_read_b64_tr_b16, 8 consecutive k of one row) than the 128 x 64
-// sub-tiles of the 256 x 256 kernel. On the 48 layers of a 12-block
-// transformer step (d = 768 / 3072, B = 128, T = 256) it is 3-4 % faster
-// than that kernel. What bounds both (measured with variants that
-// drop one part at a time): the MFMA issue of this loop on its own reaches
-// about 1.35 PFLOP/s, the copies and the per-slice barrier add the rest, and
-// with random bf16 data the matrix cores sustain about 1.9 PFLOP/s at the
-// power limit rather than the nominal 2.5.
+// Why a second tile shape: per FLOP a 384 x 256 workgroup tile copies 17 %
+// fewer bytes into LDS than a 256 x 256 one. Sixteen waves (four per SIMD) own
+// 96 x 64 sub-tiles (96 fp32 accumulators each), so a wave that waits on LDS
+// reads or the slice barrier leaves three others to keep its SIMD's matrix
+// core busy; the transposed reads per FLOP (ds_read_b64_tr_b16, 8 consecutive
+// k of one row) are 12 % more than with 128 x 64 sub-tiles, but the LDS is far
+// from saturated in this loop (the LDS-activity counter reads about two
+// cycles per transposed read). On the 48 layers of a 12-block transformer
+// step (d = 768 / 3072, B = 128, T = 256): 5.56-5.58 ms against 5.73 ms for
+// eight waves with 96 x 128 sub-tiles and 6.0-6.2 ms for the 256 x 256
+// kernel. Measured bounds: the MFMA issue of the eight-wave loop on its own
+// reached about 1.35 PFLOP/s, and with random bf16 data the matrix cores
+// sustain about 1.9 PFLOP/s at the power limit rather than the nominal 2.5.
 //
-// Layout of one ring slot (40 KB): the G slice (32 k-rows of 384 bf16) then
-// the A slice (32 k-rows of 256 bf16). Both are stored in 256-byte units that
+// Layout of one ring slot (80 KB): the G slice (64 k-rows of 384 bf16) then
+// the A slice (64 k-rows of 256 bf16). Both are stored in 256-byte units that
 // hold one 64-byte column block of four consecutive k-rows (k-row 4 q + r at
 // byte 64 r of the unit); units run along the columns, then along q. Each
 // global_load_lds_dwordx4 fills 1 KB of the slot (four units) in order: lane
@@ -44,26 +46,30 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kWdTM = 384;                      // tile rows (d_out)
 constexpr int kWdTN = 256;                      // tile columns (d_in)
-constexpr int kWdBK = 32;                       // k rows per slice
-constexpr int kWdWaves = 8;                     // 4 (M) x 2 (N) waves
+constexpr int kWdBK = 64;                       // k rows per slice
+constexpr int kWdWaves = 16;                    // 4 (M) x 4 (N) waves
+constexpr int kWdWavesN = 4;
 constexpr int kWdThreads = 64 * kWdWaves;
 constexpr int kWdMB = 3;                        // 32-row blocks per wave
-constexpr int kWdNB = 4;                        // 32-column blocks per wave
+constexpr int kWdNB = 2;                        // 32-column blocks per wave
 constexpr int kWdGGroup = 4 * kWdTM * 2;        // 3 KB: four G k-rows (12 units)
 constexpr int kWdAGroup = 4 * kWdTN * 2;        // 2 KB: four A k-rows (8 units)
-constexpr int kWdGBytes = kWdBK / 4 * kWdGGroup;   // 24 KB
-constexpr int kWdABytes = kWdBK / 4 * kWdAGroup;   // 16 KB
+constexpr int kWdGBytes = kWdBK / 4 * kWdGGroup;   // 48 KB
+constexpr int kWdABytes = kWdBK / 4 * kWdAGroup;   // 32 KB
 constexpr int kWdStageBytes = kWdGBytes + kWdABytes;
 // Two ring slots: the next slice's copies run while the current one is
-// multiplied. Measured on the 48-layer step: 2 slots 5.63 ms, 3 slots 6.04,
-// 4 slots 5.78-5.83 (more bytes in flight do not help; 64-row slices in two
-// 80 KB slots, which halve the barriers, also gave 5.62-5.63).
+// multiplied. With eight waves and 32-row slices, two 40 KB slots measured
+// 5.63 ms on the 48-layer step against 6.04 for three and 5.78-5.83 for four
+// (more bytes in flight did not help).
 constexpr int kWdStages = 2;
-constexpr int kWdLdsBytes = kWdStages * kWdStageBytes;   // 80 KB
-constexpr int kWdGCopies = kWdGBytes / 1024;             // 24
+constexpr int kWdLdsBytes = kWdStages * kWdStageBytes;   // 160 KB
+constexpr int kWdGCopies = kWdGBytes / 1024;             // 48
 constexpr int kWdCopies = kWdStageBytes / 1024 / kWdWaves;  // 5 per wave per slice
 constexpr int kWdTileElems = kWdTM * kWdTN;
 static_assert(kWdGCopies % kWdWaves == 0, "G copies split evenly over the waves");
+static_assert((kWdStageBytes / 1024) % kWdWaves == 0, "copies split evenly over the waves");
+static_assert(kWdWaves / kWdWavesN * kWdMB * 32 == kWdTM && kWdWavesN * kWdNB * 32 == kWdTN,
+              "the wave grid covers the tile");
 static_assert(kWdLdsBytes <= 160 * 1024, "LDS budget");
 static_assert(kWdStages >= 2, "the ring needs a slot being filled and one being read");
 
@@ -133,8 +139,8 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
   typedef __attribute__((address_space(4))) const float const_float;
   const const_float* fac = (const const_float*)factors;
 
-  // Copy p of this wave is copy t = wave + 8 p of the slot. For G (t < 24)
-  // it fills row group t / 3, column blocks 4 (t % 3) .. +3; for A (u = t - 24)
+  // Copy p of this wave is copy t = wave + 16 p of the slot. For G (t < 48)
+  // it fills row group t / 3, column blocks 4 (t % 3) .. +3; for A (u = t - 48)
   // row group u / 2, column blocks 4 (u % 2) .. +3. Lane i writes unit i / 16,
   // k-row (i % 16) / 4 of the group, bytes 16 (i % 4) .. +15 of the block.
   const uint32_t l_unit = (uint32_t)lane >> 4, l_row = ((uint32_t)lane >> 2) & 3u,
@@ -167,7 +173,7 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
 #pragma unroll
     for (int p = 0; p < kWdCopies; ++p) {
       const int t = (int)wave_u + kWdWaves * p;
-      // t < 24 exactly for p < 3 (24 = 3 * 8): the operand is known per p.
+      // t < 48 exactly for p < 3 (48 = 3 * 16): the operand is known per p.
       if (p < kWdGCopies / kWdWaves)
         copy16_to_lds(gs, zero ? zoff : voff[p], dst + 1024u * (uint32_t)t);
       else
@@ -180,7 +186,7 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
   // 8 (g / 2) + 4 h + s / 4, i.e. row group 2 (g / 2) + h and row s / 4 of
   // it, at byte 32 (g & 1) + 8 (s % 4) of the wave's first column block. Block
   // i and k-step ks add 256 i and 16 rows (4 row groups) as immediates.
-  const int wave = (int)wave_u, wm = wave >> 1, wn = wave & 1;
+  const int wave = (int)wave_u, wm = wave / kWdWavesN, wn = wave % kWdWavesN;
   const int g = lane >> 4, s = lane & 15;
   uint32_t rg[2], ra[2];
 #pragma unroll
@@ -258,12 +264,13 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
 
 // Writes scale * acc into a 384 x 256 row-major destination (row stride ld),
 // adding what is there when add. Register v of block (i, j) in lane l is tile
-// row 96 wm + 32 i + 8 (v / 4) + 4 (l / 32) + v % 4, column 128 wn + 32 j + l % 32.
+// row 32 (kWdMB wm + i) + 8 (v / 4) + 4 (l / 32) + v % 4, column 32 (kWdNB wn + j) + l % 32.
 __device__ __forceinline__ void wd_store(float* dst, int64_t ld, const WdAcc& acc, float scale,
                                          bool add) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  float* p0 = dst + (int64_t)(wm * 96 + 4 * (lane >> 5)) * ld + wn * 128 + (lane & 31);
+  const int wm = wave / kWdWavesN, wn = wave % kWdWavesN;
+  float* p0 = dst + (int64_t)(wm * kWdMB * 32 + 4 * (lane >> 5)) * ld + wn * kWdNB * 32 +
+              (lane & 31);
 #pragma unroll
   for (int i = 0; i < kWdMB; ++i)
 #pragma unroll

@@ -214,7 +214,7 @@ CLIP_SHAPES = [
     (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
     (8, 256, 256, 256, wl.BF16),    # 256x256-tile kernel, split along K
     (4, 64, 256, 384, wl.BF16),     # 384x256-tile kernel, one tile split along K
-    (3, 96, 512, 768, wl.BF16),     # 384x256-tile kernel, four tiles, 3 slices per example
+    (3, 128, 512, 768, wl.BF16),    # 384x256-tile kernel, four tiles, 2 slices per example
     (8, 256, 256, 384, wl.BF16),    # 384x256-tile kernel, d_out not a multiple of 256, long K
 ]
 TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-5:]
