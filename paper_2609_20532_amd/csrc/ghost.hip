@@ -240,7 +240,10 @@ __global__ __launch_bounds__(kGhThreads, 2) void ghost_dma_kernel(GhArgs args) {
 // or G. In LDS a row takes 128 bytes and its 16-byte chunk c sits at slot
 // c ^ ((row >> 1) & 7), which keeps the 16-lane operand reads conflict-free.
 
-constexpr int kGgThreads = 512;
+constexpr int kGgWaves = 8;                          // 4 column groups x kGgWavesM row groups
+constexpr int kGgThreads = 64 * kGgWaves;
+constexpr int kGgWavesM = kGgWaves / 4;
+constexpr int kGgRB = kGhRows / 32 / kGgWavesM;     // 32-row blocks per wave
 constexpr int kGgBK = 64;
 constexpr int kGgStages = 4;
 constexpr int kGgBlockBytes = kGhRows * kGgBK * 2;   // 16 KB: one row block of a slice
@@ -266,7 +269,7 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 2, wn = wave & 3;   // wm < kGgWavesM
   const int T = E.T;
   const int rows_a = min(kGhRows, T - kGhRows * a);
   const int rows_b = min(kGhRows, T - kGhRows * b);
@@ -275,15 +278,15 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
   const char* Gb = static_cast<const char*>(E.G) + i * (int64_t)T * E.d_out * 2;
   const uint32_t lds0 = lds_address(lds);
 
-  // Copy u of this wave moves rows 8 j .. 8 j + 7 (j = wave + 8 u) of the
+  // Copy u of this wave moves rows 8 j .. 8 j + 7 (j = wave + waves u) of the
   // 256-row window of blocks a and b: lane l takes row 8 j + l / 8 and the
   // global chunk that belongs in its slot l % 8. Rows past T repeat the last
   // row (in-bounds; masked out of the sum).
-  constexpr int kCopies = 4;
+  constexpr int kCopies = 32 / kGgWaves;
   uint32_t offA[kCopies], offG[kCopies];
 #pragma unroll
   for (int u = 0; u < kCopies; ++u) {
-    const int j = (int)wave_u + 8 * u;
+    const int j = (int)wave_u + kGgWaves * u;
     const int row = min(kGhRows * a + 8 * j + (lane >> 3), T - 1);
     const int chunk = (lane & 7) ^ ((4 * (j & 1) + (lane >> 4)) & 7);
     offA[u] = (uint32_t)row * (uint32_t)E.d_in * 2u + 16u * chunk;
@@ -295,7 +298,7 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
     const uint32_t dst = lds0 + (uint32_t)slot * kGgStageBytes;
 #pragma unroll
     for (int u = 0; u < kCopies; ++u)
-      copy16_to_lds(src, isA ? offA[u] : offG[u], dst + 1024u * ((int)wave_u + 8 * u));
+      copy16_to_lds(src, isA ? offA[u] : offG[u], dst + 1024u * ((int)wave_u + kGgWaves * u));
   };
 
   // Operand reads: lane l supplies row (l % 32) of a 32-row block and chunk
@@ -304,22 +307,22 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
   uint32_t rd[4];
 #pragma unroll
   for (int st = 0; st < 4; ++st) rd[st] = (lane & 31) * 128 + 16 * ((2 * st + g) ^ f);
-  const uint32_t rowsA = 64 * wm * 128, rowsB = kGgBlockBytes + 64 * wm * 128;
+  const uint32_t rowsA = 32 * kGgRB * wm * 128, rowsB = kGgBlockBytes + 32 * kGgRB * wm * 128;
   const uint32_t colA = 32 * wn * 128, colB = kGgBlockBytes + 32 * wn * 128;
 
-  // Tiles t = 0: (a, a), 1: (a, b), 2: (b, b); each wave: rows 64 wm .. +63
-  // (two 32-row blocks r) and columns 32 wn .. +31 of every tile.
-  f32x16_t accA[3][2], accG[3][2];
+  // Tiles t = 0: (a, a), 1: (a, b), 2: (b, b); each wave: rows 32 kGgRB wm ..
+  // (kGgRB 32-row blocks r) and columns 32 wn .. +31 of every tile.
+  f32x16_t accA[3][kGgRB], accG[3][kGgRB];
 #pragma unroll
   for (int t = 0; t < 3; ++t)
 #pragma unroll
-    for (int r = 0; r < 2; ++r) accA[t][r] = accG[t][r] = f32x16_t{};
+    for (int r = 0; r < kGgRB; ++r) accA[t][r] = accG[t][r] = f32x16_t{};
 
 #pragma unroll
   for (int d = 0; d < kGgStages - 1; ++d)
     if (d < n) issue(d, d);
 
-  auto slice = [&](int s, f32x16_t (&acc)[3][2]) {
+  auto slice = [&](int s, f32x16_t (&acc)[3][kGgRB]) {
     // This wave's copies of slice s have landed once at most the later
     // slices' copies are outstanding; the barrier makes every wave's part
     // visible and guarantees slice s - 1, whose slot is refilled next, is no
@@ -334,16 +337,16 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
     const char* base = lds + (s % kGgStages) * kGgStageBytes;
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      bf16x8_t fa[2], fb[2];
+      bf16x8_t fa[kGgRB], fb[kGgRB];
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
+      for (int r = 0; r < kGgRB; ++r) {
         fa[r] = *(lds_frag*)(base + rowsA + 4096 * r + rd[st]);
         fb[r] = *(lds_frag*)(base + rowsB + 4096 * r + rd[st]);
       }
       const bf16x8_t ca = *(lds_frag*)(base + colA + rd[st]);
       const bf16x8_t cb = *(lds_frag*)(base + colB + rd[st]);
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
+      for (int r = 0; r < kGgRB; ++r) {
         acc[0][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], ca, acc[0][r], 0, 0, 0);
         acc[1][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], cb, acc[1][r], 0, 0, 0);
         acc[2][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[r], cb, acc[2][r], 0, 0, 0);
@@ -353,18 +356,18 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
   for (int s = 0; s < nA; ++s) slice(s, accA);
   for (int s = nA; s < n; ++s) slice(s, accG);
 
-  // Element v of block r in lane l: tile row 64 wm + 32 r + 8 (v / 4) + 4 (l / 32)
-  // + v % 4, column 32 wn + l % 32.
+  // Element v of block r in lane l: tile row 32 (kGgRB wm + r) + 8 (v / 4) +
+  // 4 (l / 32) + v % 4, column 32 wn + l % 32.
   float sum[3] = {0.f, 0.f, 0.f};
   const int col = 32 * wn + (lane & 31);
 #pragma unroll
   for (int t = 0; t < 3; ++t) {
     const int rv = t == 2 ? rows_b : rows_a, cv = t == 0 ? rows_a : rows_b;
 #pragma unroll
-    for (int r = 0; r < 2; ++r)
+    for (int r = 0; r < kGgRB; ++r)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = 64 * wm + 32 * r + 8 * (v >> 2) + 4 * g + (v & 3);
+        const int row = 32 * (kGgRB * wm + r) + 8 * (v >> 2) + 4 * g + (v & 3);
         const float x = accA[t][r][v] * accG[t][r][v];
         sum[t] += (row < rv && col < cv) ? x : 0.f;
       }
