@@ -90,6 +90,28 @@ struct TrClipPlan {
   int64_t n_tiles = 0, n_full = 0, n_tail = 0, Q = 0, tail_w = 1;
   size_t tail_bytes = 0;  // tail partials in the workspace
 };
+// K ranges that each of the rem leftover tiles (rem < cus) of a whole-tile
+// launch is split into; 1 leaves them whole. Unsplit they take one round of
+// whole-tile time; split w ways they take ceil(rem w / cus) rounds of 1 / w of
+// it, plus the traffic of rem w partial tiles written and read back by the
+// fixup. The estimate prices a tile's flops at a sustained per-CU matrix rate
+// and the partial bytes at a sustained HBM rate; ties keep the smaller w.
+inline int64_t choose_tail_split(int64_t rem, int64_t cus, int64_t Q, double tile_flops,
+                                 double tile_bytes) {
+  constexpr double kCuFlops = 4.0e12;   // flop/s of one CU in these kernels
+  constexpr double kHbm = 5.0e12;       // B/s for the partial writes and reads
+  constexpr int64_t kMaxSplit = 16;
+  if (rem <= 0 || cus <= 0) return 1;
+  const double t_tile = tile_flops / kCuFlops;
+  double best = t_tile;
+  int64_t w_best = 1;
+  for (int64_t w = 2; w <= kMaxSplit && w <= Q; ++w) {
+    const int64_t rounds = (rem * w + cus - 1) / cus;
+    const double t = (double)rounds / (double)w * t_tile + 2.0 * (double)(rem * w) * tile_bytes / kHbm;
+    if (t < best) { best = t; w_best = w; }
+  }
+  return w_best;
+}
 void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan);
 int launch_tr_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
                    float* const* outs, int accumulate, const TrClipPlan& plan, float* tail_ws,

@@ -284,7 +284,7 @@ __global__ __launch_bounds__(kTrThreads, 1) void tgemm_tr_kernel(TrArgs args) {
   TrLane ln;
   init_lane(ln, lane);
   TrAcc acc;
-  const uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x);
+  const uint32_t job = xcd_two_class_index(blockIdx.x, gridDim.x, args.n_full);
 
   if (EPI == TR_SUMSQ) {
     // job -> (layer, example, tile); jobs of a layer are B * tiles, laid out from tile_begin * B
@@ -440,8 +440,8 @@ void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrC
   // the CUs (only when every tile has the same Q).
   const int64_t rem = tiles % cus;
   if (uniform && n > 0 && rem != 0) {
-    int64_t w = cus / rem;
-    if (w > Q) w = Q;
+    const double tile_flops = 2.0 * kTrTile * kTrTile * (double)(Q * kTrBK);
+    const int64_t w = choose_tail_split(rem, cus, Q, tile_flops, 4.0 * kTrTile * kTrTile);
     if (w > 1) {
       plan->n_full = tiles - rem;
       plan->tail_w = w;

@@ -14,9 +14,11 @@
 // cycles per transposed read). On the 48 layers of a 12-block transformer
 // step (d = 768 / 3072, B = 128, T = 256): 5.56-5.58 ms against 5.73 ms for
 // eight waves with 96 x 128 sub-tiles and 6.0-6.2 ms for the 256 x 256
-// kernel. Measured bounds: the MFMA issue of the eight-wave loop on its own
-// reached about 1.35 PFLOP/s, and with random bf16 data the matrix cores
-// sustain about 1.9 PFLOP/s at the power limit rather than the nominal 2.5.
+// kernel; with the whole tiles and the split-K tail spread evenly over the
+// XCDs (xcd_two_class_index) 4.92-4.98 ms. Measured bounds: the MFMA issue of
+// the eight-wave loop on its own reached about 1.35 PFLOP/s, and with random
+// bf16 data the matrix cores sustain about 1.9 PFLOP/s at the power limit
+// rather than the nominal 2.5.
 //
 // Layout of one ring slot (80 KB): the G slice (64 k-rows of 384 bf16) then
 // the A slice (64 k-rows of 256 bf16). Both are stored in 256-byte units that
@@ -292,7 +294,7 @@ __global__ __launch_bounds__(kWdThreads, 1) void tgemm_wide_kernel(WdArgs args) 
   __shared__ __attribute__((aligned(1024))) char lds[kWdLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   WdAcc acc;
-  const uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x);
+  const uint32_t job = xcd_two_class_index(blockIdx.x, gridDim.x, args.n_full);
   const bool whole = job < args.n_full;
   uint32_t tile_g = job, qa = 0, qb = 0;
   if (!whole) {
@@ -381,8 +383,8 @@ void plan_wide_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, T
   plan->tail_w = 1;
   const int64_t rem = tiles % cus;
   if (uniform && n > 0 && rem != 0) {
-    int64_t w = cus / rem;
-    if (w > Q) w = Q;
+    const double tile_flops = 2.0 * kWdTM * kWdTN * (double)(Q * kWdBK);
+    const int64_t w = choose_tail_split(rem, cus, Q, tile_flops, 4.0 * kWdTileElems);
     if (w > 1) {
       plan->n_full = tiles - rem;
       plan->tail_w = w;

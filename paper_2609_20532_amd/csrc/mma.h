@@ -169,6 +169,23 @@ __device__ __forceinline__ uint32_t xcd_logical_index(uint32_t bid, uint32_t nwg
   return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
 }
 
+// xcd_logical_index for a job list of n_first jobs of one kind (whole tiles)
+// followed by jobs of another (split tail ranges): every XCD receives an even
+// share of each kind, its first-kind jobs as one contiguous range and
+// dispatched first, then its share of the rest. With a plain contiguous split
+// the first XCDs would hold only whole tiles and finish last.
+__device__ __forceinline__ uint32_t xcd_two_class_index(uint32_t bid, uint32_t nwg,
+                                                        uint32_t n_first) {
+  const uint32_t xcd = bid & 7u, idx = bid >> 3;
+  const uint32_t per = nwg >> 3, rem = nwg & 7u;
+  const uint32_t fper = n_first >> 3, frem = n_first & 7u;
+  const uint32_t f_cnt = fper + (xcd < frem ? 1u : 0u);
+  const uint32_t f_begin = xcd * fper + (xcd < frem ? xcd : frem);
+  if (idx < f_cnt) return f_begin + idx;
+  const uint32_t begin = xcd * per + (xcd < rem ? xcd : rem);
+  return n_first + (begin - f_begin) + (idx - f_cnt);
+}
+
 // Element loads for the non-vector paths.
 __device__ __forceinline__ float load_elem(const uint16_t* p) { return bf16_to_f32(*p); }
 __device__ __forceinline__ float load_elem(const float* p) { return *p; }
