@@ -252,7 +252,11 @@ constexpr int kGgLdsBytes = kGgStages * kGgStageBytes;
 
 __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args) {
   __shared__ __attribute__((aligned(1024))) char lds[kGgLdsBytes];
-  const uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x);
+  // One job reads all rows of its (example, layer) and no job shares them, so
+  // L2 locality does not matter here: the plain order deals every eighth
+  // example of each layer to each XCD, which keeps the XCDs' work equal even
+  // though the layers' widths differ.
+  const uint32_t job = blockIdx.x;
   int l = 0;
   {
     int lo = 0, hi = args.n - 1;
@@ -269,7 +273,15 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int wm = wave >> 2, wn = wave & 3;   // wm < kGgWavesM
+  // The two diagonal tiles need only their 32 x 32 blocks on or above the
+  // diagonal (row block <= column block; a block below it has the sum of its
+  // mirror), which leaves more work to the right-hand column groups. Waves w
+  // and w + 4 share a SIMD: pairing row group 0 with column group w % 4 and
+  // row group 1 with column group 3 - w % 4 gives the SIMDs 10, 10, 8 and 8
+  // blocks per k step instead of 6, 8, 10 and 12.
+  static_assert(kGgWaves == 8 && kGgRB == 2, "the pairing assumes a 2 x 4 wave grid");
+  const int wm = (int)(wave_u >> 2);
+  const int wn = wm == 0 ? (int)(wave_u & 3u) : 3 - (int)(wave_u & 3u);
   const int T = E.T;
   const int rows_a = min(kGhRows, T - kGhRows * a);
   const int rows_b = min(kGhRows, T - kGhRows * b);
@@ -347,9 +359,10 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
       const bf16x8_t cb = *(lds_frag*)(base + colB + rd[st]);
 #pragma unroll
       for (int r = 0; r < kGgRB; ++r) {
-        acc[0][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], ca, acc[0][r], 0, 0, 0);
+        const bool upper = kGgRB * wm + r <= wn;   // wave-uniform
+        if (upper) acc[0][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], ca, acc[0][r], 0, 0, 0);
         acc[1][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[r], cb, acc[1][r], 0, 0, 0);
-        acc[2][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[r], cb, acc[2][r], 0, 0, 0);
+        if (upper) acc[2][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[r], cb, acc[2][r], 0, 0, 0);
       }
     }
   };
@@ -364,13 +377,20 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
   for (int t = 0; t < 3; ++t) {
     const int rv = t == 2 ? rows_b : rows_a, cv = t == 0 ? rows_a : rows_b;
 #pragma unroll
-    for (int r = 0; r < kGgRB; ++r)
+    for (int r = 0; r < kGgRB; ++r) {
+      float blk = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = 32 * (kGgRB * wm + r) + 8 * (v >> 2) + 4 * g + (v & 3);
         const float x = accA[t][r][v] * accG[t][r][v];
-        sum[t] += (row < rv && col < cv) ? x : 0.f;
+        blk += (row < rv && col < cv) ? x : 0.f;
       }
+      // Diagonal tiles: a block above the diagonal stands for itself and its
+      // mirror; blocks below it were not computed.
+      const int R = kGgRB * wm + r;
+      const float wgt = t == 1 ? 1.f : (R < wn ? 2.f : (R == wn ? 1.f : 0.f));
+      sum[t] += wgt * blk;
+    }
     sum[t] = wave_sum(sum[t]);
   }
   __syncthreads();   // the ring is free again
