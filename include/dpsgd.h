@@ -145,6 +145,38 @@ int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Norms, factors and clipped sum in one call.  Paper: Section 2.2 (the
+ * per-example norm over all layers, the clip factor and the sum of the
+ * clipped gradients); GPU-side algorithm, clip and average steps.
+ *
+ *   norms_sq[i] = sum_l ||G_i^T A_i||_F^2            (float32 [B], overwritten)
+ *   c_i, mask_i as in dpsgd_clip_factors(norms_sq, B, C)
+ *   grads[l]    = (accumulate ? grads[l] : 0) + sum_i c_i G_i^T A_i
+ *
+ * the same results as dpsgd_per_example_norms_multi(..., accumulate = 0)
+ * followed by dpsgd_clip_accumulate_multi, within float32 rounding. A layer
+ * whose narrow side min(d_in, d_out) is at most 16 (a low-rank adapter
+ * matrix), whose wide side is a multiple of 16 bytes and whose per-example
+ * gradient (4 d_in d_out bytes) is at most a quarter of its per-example input
+ * bytes (T (d_in + d_out) element bytes) is read once: every G_i^T A_i is
+ * formed in float32 and stored in the workspace, its squared norm is summed
+ * from the stored values and the clipped sum is formed from them. Other layers
+ * use the kernels of the separate calls. mode applies to the other layers;
+ * DPSGD_NORM_GHOST also turns the stored form off. workspace: at least
+ * dpsgd_clipped_sum_workspace_bytes(layers, n_layers, mode) bytes (device,
+ * 16-byte aligned; DPSGD_ERR_INVALID_ARG otherwise).
+ * factors_out / mask_out are optional. Errors as in the two separate calls;
+ * norms_sq must not be NULL.
+ * ------------------------------------------------------------------------- */
+size_t dpsgd_clipped_sum_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers,
+                                         int32_t mode);
+
+int dpsgd_clipped_sum_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode, float C,
+                            float* const* grads, int32_t accumulate, float* norms_sq,
+                            float* factors_out, uint8_t* mask_out, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Noise.  Paper: Section 2.2, z_t ~ N(0, sigma^2 C^2 I) and
  * g_tilde = (1/|B_t|)(sum + z_t); GPU-side algorithm, noise step
  * (g_tilde = g_bar + Noise(s_noise,t; sigma C)/B).

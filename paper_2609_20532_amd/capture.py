@@ -197,7 +197,8 @@ def synthetic_tokens(cfg: GPT2Config, B: int, T: int, seed: int, device) -> torc
 def bench(B: int = 64, T: int = 128, steps: int = 10, warmup: int = 3, dtype: str = "f32") -> dict:
     """Times, on cuda:0, one capture (forward + backward of the GPT-2-small
     LoRA model) and the DP-SGD step on the captured tensors (per-example norms,
-    clip + clipped sum, noise), each averaged over ``steps`` repetitions."""
+    clip + clipped sum, noise), each averaged over ``steps`` repetitions; the
+    step as the fused call (dp_step_ms) and as the three separate calls."""
     import numpy as np
 
     from . import dpsgd
@@ -210,7 +211,7 @@ def bench(B: int = 64, T: int = 128, steps: int = 10, warmup: int = 3, dtype: st
     def events():
         return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
-    cap_ms, step_ms = [], []
+    cap_ms, step_ms, sep_ms = [], [], []
     for it in range(warmup + steps):
         e0, e1 = events()
         e0.record()
@@ -220,21 +221,29 @@ def bench(B: int = 64, T: int = 128, steps: int = 10, warmup: int = 3, dtype: st
             layers = [CapturedLayer(L.name, L.A.to(torch.bfloat16), L.G.to(torch.bfloat16), L.param)
                       for L in layers]
         Ls = [dpsgd.make_layer(L.A, L.G, k) for k, L in enumerate(layers)]
-        buf = dpsgd.alloc_step(Ls)
+        buf = dpsgd.alloc_step(Ls, fused=True)
         torch.cuda.synchronize()
+        # The step as one fused call (adapter matrices read once) plus the
+        # noise, then as the three separate calls.
         s0, s1 = events()
         s0.record()
-        dpsgd.run_step(Ls, buf, 1.0, 0.6679, 7, it, 1.0 / B)
+        dpsgd.run_step(Ls, buf, 1.0, 0.6679, 7, it, 1.0 / B, fused=True)
         s1.record()
+        p0, p1 = events()
+        p0.record()
+        dpsgd.run_step(Ls, buf, 1.0, 0.6679, 7, it, 1.0 / B)
+        p1.record()
         torch.cuda.synchronize()
         if it >= warmup:
             cap_ms.append(e0.elapsed_time(e1))
             step_ms.append(s0.elapsed_time(s1))
+            sep_ms.append(p0.elapsed_time(p1))
     in_bytes = sum(L.A.numel() * L.A.element_size() + L.G.numel() * L.G.element_size()
                    for L in layers)
-    c, s = float(np.mean(cap_ms)), float(np.mean(step_ms))
+    c, s, sp = float(np.mean(cap_ms)), float(np.mean(step_ms)), float(np.mean(sep_ms))
     return {"model": "GPT-2 small shape, LoRA r=4 alpha=8 on every c_attn (24 trainable matrices)",
             "B": B, "T": T, "dtype": dtype, "capture_ms": c, "dp_step_ms": s,
+            "dp_step_ms_separate_calls": sp,
             "dp_step_fraction": s / (c + s), "captured_bytes": in_bytes,
             "dp_step_input_gbs": in_bytes / (s * 1e-3) / 1e9,
             "dp_examples_per_s": B / (s * 1e-3), "examples_per_s_with_capture": B / ((c + s) * 1e-3)}

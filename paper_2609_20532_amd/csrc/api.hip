@@ -82,6 +82,49 @@ size_t clip_ws_bytes(const dpsgd_layer* layers, int32_t n) {
 
 bool bad_float(float x) { return isnan(x); }
 
+// Plan of dpsgd_clipped_sum_multi. Workspace: norm partials [B][P], then the
+// clip workspace of the other layers (factors first), then the stored
+// per-example gradients of the FORM_STORED layers.
+struct StepPlan {
+  NormPlan norms;
+  std::vector<int> stored, other;       // layer indices
+  std::vector<int64_t> splits;          // per stored layer
+  std::vector<size_t> store_off;        // per stored layer, from the store base
+  std::vector<dpsgd_layer> other_layers;
+  size_t clip_off = 0, store_base = 0, total = 0;
+};
+
+StepPlan plan_step(const dpsgd_layer* layers, int32_t n, int32_t mode) {
+  StepPlan p;
+  p.norms.forms.resize(n);
+  p.norms.cols.resize(n);
+  for (int32_t l = 0; l < n; ++l) {
+    const bool stored = mode != DPSGD_NORM_GHOST && skinny_ok(layers[l]);
+    p.norms.forms[l] = stored ? FORM_STORED : resolve_norm_form(layers[l], mode);
+    p.norms.cols[l] = p.norms.P;
+    p.norms.P += norm_partials_per_example(layers[l], p.norms.forms[l]);
+    (stored ? p.stored : p.other).push_back(l);
+  }
+  const int64_t B = layers[0].B;
+  p.norms.bytes = round_up((size_t)B * (size_t)p.norms.P * sizeof(float), 256);
+  for (int l : p.other) p.other_layers.push_back(layers[l]);
+  const size_t clip = p.other.empty()
+                          ? round_up((size_t)B * sizeof(float), kFactorBytesAlign)
+                          : clip_ws_bytes(p.other_layers.data(), (int32_t)p.other.size());
+  p.splits.resize(p.stored.size());
+  if (!p.stored.empty())
+    plan_skinny(layers, p.stored.data(), (int)p.stored.size(), tr_cu_count(), p.splits.data());
+  size_t store = 0;
+  for (size_t k = 0; k < p.stored.size(); ++k) {
+    p.store_off.push_back(store);
+    store += skinny_store_bytes(layers[p.stored[k]], p.splits[k]);
+  }
+  p.clip_off = p.norms.bytes;
+  p.store_base = p.clip_off + round_up(clip, 256);
+  p.total = p.store_base + store;
+  return p;
+}
+
 }  // namespace
 }  // namespace dpsgd
 
@@ -184,6 +227,75 @@ int dpsgd_clip_accumulate(const dpsgd_layer* layer, const float* norms_sq, float
   float* grads[1] = {grad};
   return dpsgd_clip_accumulate_multi(layer, 1, norms_sq, C, grads, accumulate, factors_out,
                                      mask_out, workspace, workspace_bytes, stream);
+}
+
+size_t dpsgd_clipped_sum_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers,
+                                         int32_t mode) {
+  if (check_layers(layers, n_layers, false) != DPSGD_OK || !valid_mode(mode)) return 0;
+  return plan_step(layers, n_layers, mode).total;
+}
+
+int dpsgd_clipped_sum_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode, float C,
+                            float* const* grads, int32_t accumulate, float* norms_sq,
+                            float* factors_out, uint8_t* mask_out, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  int st = check_layers(layers, n_layers, true);
+  if (st != DPSGD_OK) return st;
+  if (!valid_mode(mode)) return DPSGD_ERR_UNSUPPORTED;
+  if (!norms_sq || !grads) return DPSGD_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l)
+    if (!grads[l] || !aligned16(grads[l])) return DPSGD_ERR_INVALID_ARG;
+  if (bad_float(C) || !(C > 0.0f)) return DPSGD_ERR_INVALID_ARG;
+  const StepPlan p = plan_step(layers, n_layers, mode);
+  if (!workspace || workspace_bytes < p.total) return DPSGD_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return DPSGD_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t B = layers[0].B;
+  char* ws = static_cast<char*>(workspace);
+  float* partials = reinterpret_cast<float*>(ws);
+  float* factors = reinterpret_cast<float*>(ws + p.clip_off);
+  float* clip_partials = reinterpret_cast<float*>(
+      ws + p.clip_off + round_up((size_t)B * sizeof(float), kFactorBytesAlign));
+  std::vector<float*> stores, stored_grads;
+  for (size_t k = 0; k < p.stored.size(); ++k) {
+    stores.push_back(reinterpret_cast<float*>(ws + p.store_base + p.store_off[k]));
+    stored_grads.push_back(grads[p.stored[k]]);
+  }
+  const int n_st = (int)p.stored.size();
+
+  // Norms: the other layers' partials, the stored layers' gradients and
+  // partials, then the per-example sums.
+  if (!p.other.empty()) {
+    st = launch_norm_partials(layers, p.norms.forms.data(), n_layers, partials, p.norms.P,
+                              p.norms.cols.data(), s);
+    if (st != DPSGD_OK) return st;
+  }
+  if (n_st > 0) {
+    st = launch_skinny_norms(layers, p.stored.data(), n_st, p.norms.cols.data(), p.splits.data(),
+                             stores.data(), partials, p.norms.P, s);
+    if (st != DPSGD_OK) return st;
+  }
+  st = launch_norms_reduce(partials, p.norms.P, B, norms_sq, 0, s);
+  if (st != DPSGD_OK) return st;
+
+  // Factors, then the clipped sums.
+  st = launch_clip_factors(norms_sq, B, C, factors, factors_out, mask_out, s);
+  if (st != DPSGD_OK) return st;
+  const int n_ot = (int)p.other.size();
+  std::vector<float*> other_grads;
+  for (int l : p.other) other_grads.push_back(grads[l]);
+  for (int base = 0; base < n_ot; base += kMaxLayersPerLaunch) {
+    const int m = n_ot - base < kMaxLayersPerLaunch ? n_ot - base : kMaxLayersPerLaunch;
+    ClipPlan plan;
+    plan_clip(p.other_layers.data() + base, m, &plan);
+    st = launch_clip_sum(p.other_layers.data() + base, m, factors, other_grads.data() + base,
+                         accumulate ? 1 : 0, clip_partials, plan, s);
+    if (st != DPSGD_OK) return st;
+  }
+  if (n_st > 0)
+    return launch_skinny_clip(layers, p.stored.data(), n_st, stores.data(), factors,
+                              stored_grads.data(), accumulate ? 1 : 0, s);
+  return DPSGD_OK;
 }
 
 int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* const* grads,

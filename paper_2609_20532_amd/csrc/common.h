@@ -14,7 +14,10 @@ constexpr int kThreads = 256;          // every kernel uses 4 wave64s per workgr
 constexpr int kMaxLayersPerLaunch = 48;  // entries of a per-launch layer table (kernarg space)
 
 // Norm form actually run for a layer (T = 1 always uses the closed form).
-enum NormForm : int { FORM_T1 = 0, FORM_GHOST = 1, FORM_MAT = 2 };
+// FORM_STORED (only in dpsgd_clipped_sum_multi): per-example gradients of a
+// layer with a narrow side are formed once, stored and normed (skinny.hip).
+enum NormForm : int { FORM_T1 = 0, FORM_GHOST = 1, FORM_MAT = 2, FORM_STORED = 3 };
+constexpr int64_t kSkinnyMaxRank = 16;   // narrow side of a FORM_STORED layer
 
 // ----------------------------------------------------------- device helpers
 
@@ -72,6 +75,28 @@ NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode);
 int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
                  float* norms_sq, int accumulate, float* partials, int64_t P,
                  const int64_t* cols, hipStream_t stream);
+// The two halves of launch_norms; the partials pass skips FORM_STORED layers.
+int launch_norm_partials(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
+                         float* partials, int64_t P, const int64_t* cols, hipStream_t stream);
+int launch_norms_reduce(const float* partials, int64_t P, int64_t B, float* norms_sq,
+                        int accumulate, hipStream_t stream);
+
+// Stored per-example gradients of layers with a narrow side (skinny.hip).
+// skinny_ok: eligible (narrow side <= kSkinnyMaxRank, wide side a multiple of
+// 16 bytes, gradient at most 1/4 of the input bytes); skinny_chunks: norm
+// partials per example; plan_skinny: row ranges per layer (idx order);
+// skinny_store_bytes: the layer's store. stores[k] / outs[k] / splits[k] are
+// per position k of idx, cols per layer index.
+bool skinny_ok(const dpsgd_layer& L);
+int64_t skinny_chunks(const dpsgd_layer& L);
+void plan_skinny(const dpsgd_layer* layers, const int* idx, int n, int cus, int64_t* splits);
+size_t skinny_store_bytes(const dpsgd_layer& L, int64_t splits);
+int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                        const int64_t* splits, float* const* stores, float* partials, int64_t P,
+                        hipStream_t stream);
+int launch_skinny_clip(const dpsgd_layer* layers, const int* idx, int n, float* const* stores,
+                       const float* factors, float* const* outs, int accumulate,
+                       hipStream_t stream);
 
 // 256x256-tile bf16 kernels (gemm_tr.hip): eligibility (bf16, d_in and d_out
 // multiples of 256, T a multiple of 32), K slices of a layer, launchers.

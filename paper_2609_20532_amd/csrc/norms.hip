@@ -313,6 +313,7 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
       const int l = base + k;
       switch (forms[l]) {
         case FORM_T1: idx_t1[n_t1++] = l; break;
+        case FORM_STORED: break;   // skinny.hip
         case FORM_GHOST:
           if (ghost_dma_ok(layers[l])) idx_gd[n_gd++] = l;
           else if (ghost_vec_ok<TIn>(layers[l])) idx_gv[n_gv++] = l;
@@ -354,6 +355,7 @@ NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode) {
 int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
   switch (form) {
     case FORM_T1: return 1;
+    case FORM_STORED: return skinny_chunks(L);
     case FORM_GHOST: {
       const int64_t nt = ceil_div(L.T, kTile);
       return nt * (nt + 1) / 2;
@@ -364,18 +366,27 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
   }
 }
 
-int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers, float* norms_sq,
-                 int accumulate, float* partials, int64_t P, const int64_t* cols,
-                 hipStream_t stream) {
-  const int64_t B = layers[0].B;
-  int st = layers[0].dtype == DPSGD_BF16
-               ? launch_norms_typed<uint16_t>(layers, forms, n_layers, partials, P, cols, stream)
-               : launch_norms_typed<float>(layers, forms, n_layers, partials, P, cols, stream);
-  if (st != DPSGD_OK) return st;
+int launch_norm_partials(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
+                         float* partials, int64_t P, const int64_t* cols, hipStream_t stream) {
+  return layers[0].dtype == DPSGD_BF16
+             ? launch_norms_typed<uint16_t>(layers, forms, n_layers, partials, P, cols, stream)
+             : launch_norms_typed<float>(layers, forms, n_layers, partials, P, cols, stream);
+}
+
+int launch_norms_reduce(const float* partials, int64_t P, int64_t B, float* norms_sq,
+                        int accumulate, hipStream_t stream) {
   const int64_t wgs = ceil_div(B, 4);
   hipLaunchKernelGGL(norms_reduce_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, partials,
                      P, B, norms_sq, accumulate);
   return check_launch();
+}
+
+int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers, float* norms_sq,
+                 int accumulate, float* partials, int64_t P, const int64_t* cols,
+                 hipStream_t stream) {
+  const int st = launch_norm_partials(layers, forms, n_layers, partials, P, cols, stream);
+  if (st != DPSGD_OK) return st;
+  return launch_norms_reduce(partials, P, layers[0].B, norms_sq, accumulate, stream);
 }
 
 int launch_clip_factors(const float* norms_sq, int64_t B, float C, float* factors,

@@ -1,0 +1,411 @@
+// Per-example gradients of layers with a narrow side, formed in one pass over
+// the inputs and stored.
+//
+// A low-rank adapter matrix (LoRA, the paper's fine-tuning experiments) is a
+// linear layer whose d_in or d_out is the rank r. Its per-example gradient
+// g_i = G_i^T A_i (Section 2.2) has d_in d_out elements, far fewer than the
+// T (d_in + d_out) input elements it is formed from (GPT-2 adapters with r = 4
+// and T = 128: 32 times fewer). For such layers one pass over A and G forms
+// every g_i in float32 and stores it, the squared norm of Section 2.2 is summed
+// from the stored values, and the clip-weighted sum sum_i c_i g_i reads the
+// stored gradients instead of A and G a second time.
+//
+// Forming g_i: the wide side W (d_w = the larger of d_in, d_out) and the
+// narrow side n (r <= 16 columns) of an example are row-aligned, and
+// g_i = sum_t n_t (outer) W_t. One wave owns 64 V wide columns (16 bytes per
+// lane: V = 4 float32 or 8 bf16) and one range of rows, with r x V float32
+// sums per lane. Narrow values arrive 64 at a time, one per lane (lane L holds
+// row L / R and column L % R of a group of 64 / R rows, R = r rounded up to 4,
+// 8 or 16), and each is broadcast to the wave with v_readlane. When the
+// examples and column chunks alone give too few waves, the rows are split into
+// ranges whose partial gradients a second kernel adds in range order.
+#include "common.h"
+
+namespace dpsgd {
+namespace {
+
+constexpr int kSkWaves = kThreads / 64;   // independent waves per workgroup
+static_assert(kSkWaves == 4, "the clip kernel adds four wave sums");
+
+struct SkEntry {
+  const void* wide;      // [B][T][d_w]
+  const void* narrow;    // [B][T][r]
+  float* store;          // [splits][B][d_out * d_in]: per-example gradients (range partials)
+  int32_t T, d_w, r;
+  int32_t narrow_is_a;   // 1: the narrow side is A (d_in = r), 0: it is G (d_out = r)
+  int32_t chunks;        // wide-column chunks of 64 V
+  int32_t splits;        // row ranges per example
+  uint32_t job_begin;    // first job of this layer in the launch
+  int32_t partial_col;   // first norm-partial column (one per chunk)
+};
+
+struct SkArgs {
+  SkEntry L[kMaxLayersPerLaunch];
+  int32_t n;
+  int32_t B;
+  int64_t P;
+  float* partials;       // [B][P] norm partials
+  uint32_t jobs;         // waves of this launch
+};
+
+template <typename TIn>
+struct SkVec;
+template <>
+struct SkVec<float> {
+  static constexpr int V = 4;
+  __device__ static void cvt(const uint4& w, float (&f)[4]) {
+    f[0] = __uint_as_float(w.x);
+    f[1] = __uint_as_float(w.y);
+    f[2] = __uint_as_float(w.z);
+    f[3] = __uint_as_float(w.w);
+  }
+};
+template <>
+struct SkVec<uint16_t> {
+  static constexpr int V = 8;
+  __device__ static void cvt(const uint4& w, float (&f)[8]) {
+    f[0] = bf16_lo(w.x);
+    f[1] = bf16_hi(w.x);
+    f[2] = bf16_lo(w.y);
+    f[3] = bf16_hi(w.y);
+    f[4] = bf16_lo(w.z);
+    f[5] = bf16_hi(w.z);
+    f[6] = bf16_lo(w.w);
+    f[7] = bf16_hi(w.w);
+  }
+};
+
+__device__ __forceinline__ float sk_load(const float* p) { return *p; }
+__device__ __forceinline__ float sk_load(const uint16_t* p) { return bf16_to_f32(*p); }
+
+__device__ __forceinline__ int sk_find_layer(const SkArgs& args, uint32_t job) {
+  int lo = 0, hi = args.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.L[mid].job_begin <= job) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Offset of the lane's element (narrow column j, wide column col + v) in the
+// [d_out][d_in] gradient.
+__device__ __forceinline__ int64_t sk_offset(const SkEntry& E, int j, int col, int v) {
+  return E.narrow_is_a ? (int64_t)(col + v) * E.r + j : (int64_t)j * E.d_w + col + v;
+}
+
+// Job w of a layer: chunk w % chunks, example (w / chunks) % B, row range
+// w / (chunks B).
+template <typename TIn, int R>
+__global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
+  constexpr int V = SkVec<TIn>::V;
+  constexpr int G = 64 / R;   // rows per narrow load
+  const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
+  if (job >= args.jobs) return;   // whole waves
+  const int lane = threadIdx.x & 63;
+  const SkEntry& E = args.L[sk_find_layer(args, job)];
+  const uint32_t w = job - E.job_begin;
+  const int chunk = (int)(w % (uint32_t)E.chunks);
+  const uint32_t rest = w / (uint32_t)E.chunks;
+  const int64_t i = rest % (uint32_t)args.B;
+  const int s = (int)(rest / (uint32_t)args.B);
+  const int t0 = (int)((int64_t)E.T * s / E.splits);
+  const int t1 = (int)((int64_t)E.T * (s + 1) / E.splits);
+  const int col = (chunk * 64 + lane) * V;
+  const bool col_ok = col < E.d_w;
+  const TIn* W = static_cast<const TIn*>(E.wide) + i * E.T * (int64_t)E.d_w + (col_ok ? col : 0);
+  const TIn* Nr = static_cast<const TIn*>(E.narrow) + i * E.T * (int64_t)E.r;
+  const int nrow = lane / R, ncol = lane % R;
+
+  float acc[R][V];
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+#pragma unroll
+    for (int v = 0; v < V; ++v) acc[j][v] = 0.f;
+
+  for (int tg = t0; tg < t1; tg += G) {
+    const int rows = min(G, t1 - tg);   // wave-uniform
+    float nv = 0.f;
+    if (ncol < E.r && nrow < rows) nv = sk_load(Nr + (int64_t)(tg + nrow) * E.r + ncol);
+    uint4 wv[G];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      wv[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (u < rows && col_ok) wv[u] = *reinterpret_cast<const uint4*>(W + (int64_t)(tg + u) * E.d_w);
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      if (u < rows) {   // wave-uniform
+        float f[V];
+        SkVec<TIn>::cvt(wv[u], f);
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(nv), u * R + j));
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[j][v] = fmaf(a, f[v], acc[j][v]);
+        }
+      }
+    }
+  }
+
+  float* dst = E.store + ((int64_t)s * args.B + i) * ((int64_t)E.d_w * E.r);
+  float sq = 0.f;
+  if (col_ok) {
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      if (j < E.r) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          dst[sk_offset(E, j, col, v)] = acc[j][v];
+          sq = fmaf(acc[j][v], acc[j][v], sq);
+        }
+      }
+    }
+  }
+  if (E.splits == 1) {
+    sq = wave_sum(sq);
+    if (lane == 0) args.partials[i * args.P + E.partial_col + chunk] = sq;
+  }
+}
+
+// Layers with several row ranges: g_i = the ranges' partials added in range
+// order, written over range 0, and its squared norm per chunk. Jobs as in the
+// grad kernel with one range.
+template <typename TIn>
+__global__ __launch_bounds__(kThreads) void skinny_finish_kernel(SkArgs args) {
+  constexpr int V = SkVec<TIn>::V;
+  const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
+  if (job >= args.jobs) return;
+  const int lane = threadIdx.x & 63;
+  const SkEntry& E = args.L[sk_find_layer(args, job)];
+  const uint32_t w = job - E.job_begin;
+  const int chunk = (int)(w % (uint32_t)E.chunks);
+  const int64_t i = w / (uint32_t)E.chunks;
+  const int col = (chunk * 64 + lane) * V;
+  const int64_t per_ex = (int64_t)E.d_w * E.r;
+  const int64_t per_split = (int64_t)args.B * per_ex;
+  float* g = E.store + i * per_ex;
+  float sq = 0.f;
+  if (col < E.d_w) {
+    for (int j = 0; j < E.r; ++j)
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const int64_t off = sk_offset(E, j, col, v);
+        float x = g[off];
+        for (int s = 1; s < E.splits; ++s) x += g[s * per_split + off];
+        g[off] = x;
+        sq = fmaf(x, x, sq);
+      }
+  }
+  sq = wave_sum(sq);
+  if (lane == 0) args.partials[i * args.P + E.partial_col + chunk] = sq;
+}
+
+// out[e] = (accumulate ? out[e] : 0) + sum_i c_i g_i[e]; examples with
+// c_i == 0 add nothing. A workgroup owns 64 groups of four elements; wave w
+// sums examples w, w + 4, w + 8, ... in order and the four wave sums are added
+// as (w0 + w1) + (w2 + w3), a fixed order (results do not depend on timing).
+struct SkClipEntry {
+  const float* store;   // [B][n] per-example gradients
+  float* out;
+  int64_t n;            // d_out * d_in
+  uint32_t wg_begin;
+};
+struct SkClipArgs {
+  SkClipEntry L[kMaxLayersPerLaunch];
+  int32_t n_layers;
+  int32_t B;
+  const float* factors;
+  int32_t accumulate;
+};
+
+__global__ __launch_bounds__(kThreads) void skinny_clip_kernel(SkClipArgs args) {
+  __shared__ float red[kSkWaves - 1][64][4];
+  int lo = 0, hi = args.n_layers - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.L[mid].wg_begin <= blockIdx.x) lo = mid; else hi = mid - 1;
+  }
+  const SkClipEntry& E = args.L[lo];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t e0 = ((int64_t)(blockIdx.x - E.wg_begin) * 64 + lane) * 4;
+  const int cnt = e0 >= E.n ? 0 : (E.n - e0 < 4 ? (int)(E.n - e0) : 4);
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+  if (cnt == 4 && (E.n & 3) == 0) {
+    // Whole groups of a layer with n % 4 == 0: 16-byte loads (every example's
+    // gradient starts 16-byte aligned), four examples in flight.
+#pragma unroll 4
+    for (int i = wave; i < args.B; i += kSkWaves) {
+      const float c = args.factors[i];
+      const float4 g = *reinterpret_cast<const float4*>(E.store + (int64_t)i * E.n + e0);
+      if (c != 0.0f) {
+        sum[0] = fmaf(c, g.x, sum[0]);
+        sum[1] = fmaf(c, g.y, sum[1]);
+        sum[2] = fmaf(c, g.z, sum[2]);
+        sum[3] = fmaf(c, g.w, sum[3]);
+      }
+    }
+  } else if (cnt > 0) {
+    for (int i = wave; i < args.B; i += kSkWaves) {
+      const float c = args.factors[i];
+      if (c == 0.0f) continue;
+      const float* g = E.store + (int64_t)i * E.n + e0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q < cnt) sum[q] = fmaf(c, g[q], sum[q]);
+    }
+  }
+  if (wave > 0)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) red[wave - 1][lane][q] = sum[q];
+  __syncthreads();
+  if (wave == 0 && cnt > 0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (q < cnt) {
+        const float v = (sum[q] + red[0][lane][q]) + (red[1][lane][q] + red[2][lane][q]);
+        E.out[e0 + q] = args.accumulate ? E.out[e0 + q] + v : v;
+      }
+    }
+  }
+}
+
+int sk_vec(const dpsgd_layer& L) { return L.dtype == DPSGD_BF16 ? 8 : 4; }
+int64_t sk_rank(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_in : L.d_out; }
+int64_t sk_wide(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_out : L.d_in; }
+double sk_grad_bytes(const dpsgd_layer& L) { return 4.0 * (double)L.d_in * (double)L.d_out; }
+double sk_input_bytes(const dpsgd_layer& L) {
+  return (double)L.T * (double)(L.d_in + L.d_out) * (L.dtype == DPSGD_BF16 ? 2.0 : 4.0);
+}
+
+template <typename TIn, int R>
+void launch_grad(const SkArgs& args, hipStream_t stream) {
+  const uint32_t wgs = (args.jobs + kSkWaves - 1) / kSkWaves;
+  hipLaunchKernelGGL((skinny_grad_kernel<TIn, R>), dim3(wgs), dim3(kThreads), 0, stream, args);
+}
+
+}  // namespace
+
+bool skinny_ok(const dpsgd_layer& L) {
+  if (sk_rank(L) > kSkinnyMaxRank) return false;
+  if (sk_wide(L) % sk_vec(L) != 0) return false;
+  // The stored gradients must be much smaller than the inputs they replace.
+  return 4.0 * sk_grad_bytes(L) <= sk_input_bytes(L);
+}
+
+int64_t skinny_chunks(const dpsgd_layer& L) { return ceil_div(sk_wide(L), 64 * sk_vec(L)); }
+
+void plan_skinny(const dpsgd_layer* layers, const int* idx, int n, int cus, int64_t* splits) {
+  int64_t base = 0;
+  for (int k = 0; k < n; ++k) base += layers[idx[k]].B * skinny_chunks(layers[idx[k]]);
+  // Enough waves for about eight per CU, with at most 16 ranges, ranges of at
+  // least 64 rows and range partials at most 1/4 of the layer's input bytes.
+  int64_t target = 1;
+  while (target < 16 && base * target < 8 * (int64_t)cus) target *= 2;
+  for (int k = 0; k < n; ++k) {
+    const dpsgd_layer& L = layers[idx[k]];
+    int64_t s = 1;
+    while (2 * s <= target && L.T / (2 * s) >= 64 &&
+           4.0 * (double)(2 * s) * sk_grad_bytes(L) <= sk_input_bytes(L))
+      s *= 2;
+    splits[k] = s;
+  }
+}
+
+size_t skinny_store_bytes(const dpsgd_layer& L, int64_t splits) {
+  return round_up((size_t)splits * (size_t)L.B * (size_t)(L.d_in * L.d_out) * sizeof(float), 256);
+}
+
+int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                        const int64_t* splits, float* const* stores, float* partials, int64_t P,
+                        hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    SkArgs ga{}, fa{};
+    ga.n = fa.n = m;
+    ga.B = fa.B = (int32_t)layers[idx[base]].B;
+    ga.P = fa.P = P;
+    ga.partials = fa.partials = partials;
+    int64_t gjobs = 0, fjobs = 0;
+    int rmax = 0;
+    bool any_split = false;
+    for (int k = 0; k < m; ++k) {
+      const dpsgd_layer& L = layers[idx[base + k]];
+      SkEntry E{};
+      E.narrow_is_a = L.d_in <= L.d_out ? 1 : 0;
+      E.wide = E.narrow_is_a ? L.G : L.A;
+      E.narrow = E.narrow_is_a ? L.A : L.G;
+      E.store = stores[base + k];
+      E.T = (int32_t)L.T;
+      E.d_w = (int32_t)sk_wide(L);
+      E.r = (int32_t)sk_rank(L);
+      E.chunks = (int32_t)skinny_chunks(L);
+      E.splits = (int32_t)splits[base + k];
+      E.partial_col = (int32_t)cols[idx[base + k]];
+      ga.L[k] = E;
+      fa.L[k] = E;
+      ga.L[k].job_begin = (uint32_t)gjobs;
+      fa.L[k].job_begin = (uint32_t)fjobs;
+      gjobs += L.B * E.chunks * E.splits;
+      // Layers with one range are finished by the grad kernel; the finish
+      // kernel gives them no jobs (a layer with none starts where the next
+      // one does and is never the one found for a job).
+      if (E.splits > 1) {
+        fjobs += L.B * E.chunks;
+        any_split = true;
+      }
+      if (E.r > rmax) rmax = E.r;
+    }
+    if (gjobs > 0x7FFFFFFF || fjobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    ga.jobs = (uint32_t)gjobs;
+    fa.jobs = (uint32_t)fjobs;
+    const bool bf16 = layers[idx[base]].dtype == DPSGD_BF16;
+    if (bf16) {
+      if (rmax <= 4) launch_grad<uint16_t, 4>(ga, stream);
+      else if (rmax <= 8) launch_grad<uint16_t, 8>(ga, stream);
+      else launch_grad<uint16_t, 16>(ga, stream);
+    } else {
+      if (rmax <= 4) launch_grad<float, 4>(ga, stream);
+      else if (rmax <= 8) launch_grad<float, 8>(ga, stream);
+      else launch_grad<float, 16>(ga, stream);
+    }
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    if (any_split) {
+      const uint32_t wgs = (fa.jobs + kSkWaves - 1) / kSkWaves;
+      if (bf16)
+        hipLaunchKernelGGL(skinny_finish_kernel<uint16_t>, dim3(wgs), dim3(kThreads), 0, stream, fa);
+      else
+        hipLaunchKernelGGL(skinny_finish_kernel<float>, dim3(wgs), dim3(kThreads), 0, stream, fa);
+      if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    }
+  }
+  return DPSGD_OK;
+}
+
+int launch_skinny_clip(const dpsgd_layer* layers, const int* idx, int n, float* const* stores,
+                       const float* factors, float* const* outs, int accumulate,
+                       hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    SkClipArgs a{};
+    a.n_layers = m;
+    a.B = (int32_t)layers[idx[base]].B;
+    a.factors = factors;
+    a.accumulate = accumulate;
+    int64_t wgs = 0;
+    for (int k = 0; k < m; ++k) {
+      const dpsgd_layer& L = layers[idx[base + k]];
+      SkClipEntry& E = a.L[k];
+      E.store = stores[base + k];
+      E.out = outs[base + k];
+      E.n = L.d_in * L.d_out;
+      E.wg_begin = (uint32_t)wgs;
+      wgs += ceil_div(E.n, 4 * 64);
+    }
+    if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(skinny_clip_kernel, dim3((uint32_t)wgs), dim3(kThreads), 0, stream, a);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
+}
+
+}  // namespace dpsgd

@@ -33,7 +33,8 @@ DPSGD_ERR_HIP = -4
 EXPORTED = (
     "dpsgd_norms_workspace_bytes", "dpsgd_select_norm_mode", "dpsgd_per_example_norms",
     "dpsgd_per_example_norms_multi", "dpsgd_clip_factors", "dpsgd_clip_workspace_bytes",
-    "dpsgd_clip_accumulate", "dpsgd_clip_accumulate_multi", "dpsgd_add_noise",
+    "dpsgd_clip_accumulate", "dpsgd_clip_accumulate_multi", "dpsgd_clipped_sum_workspace_bytes",
+    "dpsgd_clipped_sum_multi", "dpsgd_add_noise",
     "dpsgd_add_noise_multi", "dpsgd_noise_adamw", "dpsgd_noise_adamw_multi",
     "dpsgd_philox_u32", "dpsgd_gaussian", "dpsgd_status_string", "dpsgd_version",
 )
@@ -88,6 +89,9 @@ def _declare(lib):
         "dpsgd_clip_accumulate": (ctypes.c_int, [L, vp, f32, vp, i32, vp, vp, vp, sz, vp]),
         "dpsgd_clip_accumulate_multi": (ctypes.c_int,
                                         [L, i32, vp, f32, P(vp), i32, vp, vp, vp, sz, vp]),
+        "dpsgd_clipped_sum_workspace_bytes": (sz, [L, i32, i32]),
+        "dpsgd_clipped_sum_multi": (ctypes.c_int, [L, i32, i32, f32, P(vp), i32, vp, vp, vp, vp,
+                                                   sz, vp]),
         "dpsgd_add_noise": (ctypes.c_int, [L, vp, f32, f32, u64, u32, f32, vp]),
         "dpsgd_add_noise_multi": (ctypes.c_int, [L, i32, P(vp), f32, f32, u64, u32, f32, vp]),
         "dpsgd_noise_adamw": (ctypes.c_int, [L, vp, vp, vp, vp, vp, f32, f32, u64, u32, f32,
@@ -248,6 +252,24 @@ def dpsgd_clip_accumulate_multi(layers, norms_sq, C, grads, accumulate=False, fa
     _check("dpsgd_clip_accumulate_multi", st)
 
 
+def dpsgd_clipped_sum_workspace_bytes(layers, mode: int = DPSGD_NORM_AUTO) -> int:
+    load()
+    arr, n = _array(layers)
+    return int(_lib.dpsgd_clipped_sum_workspace_bytes(arr, n, mode))
+
+
+def dpsgd_clipped_sum_multi(layers, mode, C, grads, norms_sq, accumulate=False, factors_out=None,
+                            mask_out=None, workspace=None, stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_clipped_sum_multi(arr, n, mode, C, _ptr_array(grads), int(accumulate),
+                                      _ptr(norms_sq), _ptr(factors_out), _ptr(mask_out),
+                                      _ptr(workspace),
+                                      0 if workspace is None else workspace.numel(),
+                                      _stream(stream))
+    _check("dpsgd_clipped_sum_multi", st)
+
+
 def dpsgd_add_noise(layer, grad, sigma, C, seed, step, scale, stream=None):
     load()
     st = _lib.dpsgd_add_noise(ctypes.byref(layer), _ptr(grad), sigma, C, seed, step, scale,
@@ -314,14 +336,17 @@ class StepBuffers:
     norms_ws: object
     clip_ws: object
     grads: list
+    fused_ws: object = None   # workspace of dpsgd_clipped_sum_multi (alloc_step(fused=True))
 
 
-def alloc_step(layers, mode: int = DPSGD_NORM_AUTO, device="cuda") -> StepBuffers:
-    """Allocate (with torch) every buffer a step over ``layers`` needs."""
+def alloc_step(layers, mode: int = DPSGD_NORM_AUTO, device="cuda", fused: bool = False) -> StepBuffers:
+    """Allocate (with torch) every buffer a step over ``layers`` needs; with
+    ``fused`` also the workspace of the one-call form (run_step(fused=True))."""
     import torch
     B = layers[0].B
     nb = dpsgd_norms_workspace_bytes(layers, mode)
     cb = dpsgd_clip_workspace_bytes(layers)
+    fb = dpsgd_clipped_sum_workspace_bytes(layers, mode) if fused else 0
     return StepBuffers(
         norms_sq=torch.empty(B, dtype=torch.float32, device=device),
         factors=torch.empty(B, dtype=torch.float32, device=device),
@@ -330,15 +355,22 @@ def alloc_step(layers, mode: int = DPSGD_NORM_AUTO, device="cuda") -> StepBuffer
         clip_ws=torch.empty(max(cb, 1), dtype=torch.uint8, device=device),
         grads=[torch.empty((L.d_out, L.d_in), dtype=torch.float32, device=device)
                for L in layers],
+        fused_ws=torch.empty(max(fb, 1), dtype=torch.uint8, device=device) if fused else None,
     )
 
 
 def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
-             scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, stream=None):
-    """One DP-SGD gradient step: global norms, clip + sum, noise (three ABI calls)."""
-    dpsgd_per_example_norms_multi(layers, mode, buf.norms_sq, accumulate=False,
-                                  workspace=buf.norms_ws, stream=stream)
-    dpsgd_clip_accumulate_multi(layers, buf.norms_sq, C, buf.grads, accumulate=False,
+             scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, stream=None, fused: bool = False):
+    """One DP-SGD gradient step: global norms, clip + sum, noise (three ABI
+    calls, or two with ``fused``: dpsgd_clipped_sum_multi, then the noise)."""
+    if fused:
+        dpsgd_clipped_sum_multi(layers, mode, C, buf.grads, buf.norms_sq, accumulate=False,
                                 factors_out=buf.factors, mask_out=buf.mask,
-                                workspace=buf.clip_ws, stream=stream)
+                                workspace=buf.fused_ws, stream=stream)
+    else:
+        dpsgd_per_example_norms_multi(layers, mode, buf.norms_sq, accumulate=False,
+                                      workspace=buf.norms_ws, stream=stream)
+        dpsgd_clip_accumulate_multi(layers, buf.norms_sq, C, buf.grads, accumulate=False,
+                                    factors_out=buf.factors, mask_out=buf.mask,
+                                    workspace=buf.clip_ws, stream=stream)
     dpsgd_add_noise_multi(layers, buf.grads, sigma, C, seed, step, scale, stream=stream)

@@ -46,7 +46,10 @@ CONFIGS = [
 
 @pytest.mark.parametrize("name,kw,B,T", CONFIGS)
 @pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
-def test_step_on_captured_lora_tensors(dp, name, kw, B, T, dtype):
+@pytest.mark.parametrize("fused", [False, True])
+def test_step_on_captured_lora_tensors(dp, name, kw, B, T, dtype, fused):
+    """fused: norms, factors and clipped sum in one call (the adapter matrices
+    take the stored per-example gradient form), then the noise."""
     import torch
     from paper_2609_20532_amd import capture as cap
     cfg = cap.GPT2Config(**kw)
@@ -61,14 +64,14 @@ def test_step_on_captured_lora_tensors(dp, name, kw, B, T, dtype):
     nsq_ref = oracle.per_example_norms_sq(ol)
     C = float(np.median(np.sqrt(nsq_ref)))   # about half the examples clipped
     sigma, seed = 0.6679, 11
-    buf = dp.alloc_step(Ls)
-    dp.run_step(Ls, buf, C, sigma, seed, 0, 1.0 / B)
+    buf = dp.alloc_step(Ls, fused=fused)
+    dp.run_step(Ls, buf, C, sigma, seed, 0, 1.0 / B, fused=fused)
     torch.cuda.synchronize()
     res = oracle.dpsgd_step(ol, C, sigma, seed, 0, scale=1.0 / B)
     tol = TOL[dtype]
     n_gpu = np.sqrt(buf.norms_sq.cpu().numpy().astype(np.float64))
     nerr = float(np.max(np.abs(n_gpu - res.norms) / res.norms))
-    _log(f"{name} {dtype}: {len(Ls)} layers, norm err {nerr:.2e}")
+    _log(f"{name} {dtype} fused={fused}: {len(Ls)} layers, norm err {nerr:.2e}")
     assert nerr <= min(tol, 1e-4)
     band = guard_band(res.norms, C, tol)
     np.testing.assert_array_equal(buf.mask.cpu().numpy()[~band], res.mask[~band])
