@@ -45,14 +45,15 @@ struct SkArgs {
   int32_t B;
   int64_t P;
   float* partials;       // [B][P] norm partials
-  uint32_t jobs;         // waves of this launch
+  uint32_t jobs;         // waves (grad kernel) or workgroups (finish kernel)
 };
 
-template <typename TIn>
+// V wide elements per lane and row, loaded as one 16- or 8-byte access.
+template <typename TIn, int V>
 struct SkVec;
 template <>
-struct SkVec<float> {
-  static constexpr int V = 4;
+struct SkVec<float, 4> {
+  typedef uint4 raw;
   __device__ static void cvt(const uint4& w, float (&f)[4]) {
     f[0] = __uint_as_float(w.x);
     f[1] = __uint_as_float(w.y);
@@ -61,8 +62,8 @@ struct SkVec<float> {
   }
 };
 template <>
-struct SkVec<uint16_t> {
-  static constexpr int V = 8;
+struct SkVec<uint16_t, 8> {
+  typedef uint4 raw;
   __device__ static void cvt(const uint4& w, float (&f)[8]) {
     f[0] = bf16_lo(w.x);
     f[1] = bf16_hi(w.x);
@@ -72,6 +73,16 @@ struct SkVec<uint16_t> {
     f[5] = bf16_hi(w.z);
     f[6] = bf16_lo(w.w);
     f[7] = bf16_hi(w.w);
+  }
+};
+template <>
+struct SkVec<uint16_t, 4> {
+  typedef uint2 raw;
+  __device__ static void cvt(const uint2& w, float (&f)[4]) {
+    f[0] = bf16_lo(w.x);
+    f[1] = bf16_hi(w.x);
+    f[2] = bf16_lo(w.y);
+    f[3] = bf16_hi(w.y);
   }
 };
 
@@ -87,17 +98,11 @@ __device__ __forceinline__ int sk_find_layer(const SkArgs& args, uint32_t job) {
   return lo;
 }
 
-// Offset of the lane's element (narrow column j, wide column col + v) in the
-// [d_out][d_in] gradient.
-__device__ __forceinline__ int64_t sk_offset(const SkEntry& E, int j, int col, int v) {
-  return E.narrow_is_a ? (int64_t)(col + v) * E.r + j : (int64_t)j * E.d_w + col + v;
-}
-
 // Job w of a layer: chunk w % chunks, example (w / chunks) % B, row range
 // w / (chunks B).
-template <typename TIn, int R>
+template <typename TIn, int R, int V>
 __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
-  constexpr int V = SkVec<TIn>::V;
+  typedef typename SkVec<TIn, V>::raw Raw;
   constexpr int G = 64 / R;   // rows per narrow load
   const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
   if (job >= args.jobs) return;   // whole waves
@@ -126,17 +131,17 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
     const int rows = min(G, t1 - tg);   // wave-uniform
     float nv = 0.f;
     if (ncol < E.r && nrow < rows) nv = sk_load(Nr + (int64_t)(tg + nrow) * E.r + ncol);
-    uint4 wv[G];
+    Raw wv[G];
 #pragma unroll
     for (int u = 0; u < G; ++u) {
-      wv[u] = make_uint4(0u, 0u, 0u, 0u);
-      if (u < rows && col_ok) wv[u] = *reinterpret_cast<const uint4*>(W + (int64_t)(tg + u) * E.d_w);
+      wv[u] = Raw{};
+      if (u < rows && col_ok) wv[u] = *reinterpret_cast<const Raw*>(W + (int64_t)(tg + u) * E.d_w);
     }
 #pragma unroll
     for (int u = 0; u < G; ++u) {
       if (u < rows) {   // wave-uniform
         float f[V];
-        SkVec<TIn>::cvt(wv[u], f);
+        SkVec<TIn, V>::cvt(wv[u], f);
 #pragma unroll
         for (int j = 0; j < R; ++j) {
           const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(nv), u * R + j));
@@ -151,14 +156,33 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
   float sq = 0.f;
   if (col_ok) {
 #pragma unroll
-    for (int j = 0; j < R; ++j) {
-      if (j < E.r) {
+    for (int j = 0; j < R; ++j)
+      if (j < E.r)
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-          dst[sk_offset(E, j, col, v)] = acc[j][v];
-          sq = fmaf(acc[j][v], acc[j][v], sq);
-        }
-      }
+        for (int v = 0; v < V; ++v) sq = fmaf(acc[j][v], acc[j][v], sq);
+    if (!E.narrow_is_a) {
+      // Row j of the gradient holds this lane's V columns contiguously.
+#pragma unroll
+      for (int j = 0; j < R; ++j)
+        if (j < E.r)
+#pragma unroll
+          for (int v = 0; v < V; v += 4)
+            *reinterpret_cast<float4*>(dst + (int64_t)j * E.d_w + col + v) =
+                make_float4(acc[j][v], acc[j][v + 1], acc[j][v + 2], acc[j][v + 3]);
+    } else if (E.r == R) {
+      // Rows col .. col + V - 1 of r = R values each: V R contiguous floats.
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+#pragma unroll
+        for (int j = 0; j < R; j += 4)
+          *reinterpret_cast<float4*>(dst + (int64_t)(col + v) * R + j) =
+              make_float4(acc[j][v], acc[j + 1][v], acc[j + 2][v], acc[j + 3][v]);
+    } else {
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+          if (j < E.r) dst[(int64_t)(col + v) * E.r + j] = acc[j][v];
     }
   }
   if (E.splits == 1) {
@@ -168,36 +192,48 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
 }
 
 // Layers with several row ranges: g_i = the ranges' partials added in range
-// order, written over range 0, and its squared norm per chunk. Jobs as in the
-// grad kernel with one range.
-template <typename TIn>
+// order, written over range 0, and its squared norm per chunk. One workgroup
+// per (layer, example, chunk), numbered as the grad kernel's jobs with one
+// range. A chunk's elements are one run of 64 V r floats when the narrow side
+// is A (rows of r values) and r runs of 64 V floats when it is G; consecutive
+// threads take consecutive groups of four floats (every run starts 16-byte
+// aligned and holds a multiple of four).
+template <int V>
 __global__ __launch_bounds__(kThreads) void skinny_finish_kernel(SkArgs args) {
-  constexpr int V = SkVec<TIn>::V;
-  const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
-  if (job >= args.jobs) return;
-  const int lane = threadIdx.x & 63;
+  __shared__ float red[kSkWaves];
+  const uint32_t job = blockIdx.x;
   const SkEntry& E = args.L[sk_find_layer(args, job)];
   const uint32_t w = job - E.job_begin;
   const int chunk = (int)(w % (uint32_t)E.chunks);
   const int64_t i = w / (uint32_t)E.chunks;
-  const int col = (chunk * 64 + lane) * V;
   const int64_t per_ex = (int64_t)E.d_w * E.r;
   const int64_t per_split = (int64_t)args.B * per_ex;
   float* g = E.store + i * per_ex;
+  const int c0 = chunk * 64 * V;
+  const int cw = min(64 * V, E.d_w - c0);   // wide columns of this chunk
+  const int64_t run_len = E.narrow_is_a ? (int64_t)cw * E.r : cw;
+  const int64_t total = (E.narrow_is_a ? 1 : E.r) * run_len;
   float sq = 0.f;
-  if (col < E.d_w) {
-    for (int j = 0; j < E.r; ++j)
-#pragma unroll
-      for (int v = 0; v < V; ++v) {
-        const int64_t off = sk_offset(E, j, col, v);
-        float x = g[off];
-        for (int s = 1; s < E.splits; ++s) x += g[s * per_split + off];
-        g[off] = x;
-        sq = fmaf(x, x, sq);
-      }
+#pragma unroll 2
+  for (int64_t k = 4 * (int64_t)threadIdx.x; k < total; k += 4 * kThreads) {
+    const int64_t run = k / run_len;
+    const int64_t off = (E.narrow_is_a ? (int64_t)c0 * E.r : run * E.d_w + c0) + (k - run * run_len);
+    float4 x = *reinterpret_cast<const float4*>(g + off);
+    for (int sp = 1; sp < E.splits; ++sp) {
+      const float4 y = *reinterpret_cast<const float4*>(g + sp * per_split + off);
+      x.x += y.x;
+      x.y += y.y;
+      x.z += y.z;
+      x.w += y.w;
+    }
+    *reinterpret_cast<float4*>(g + off) = x;
+    sq = fmaf(x.x, x.x, sq);
+    sq = fmaf(x.y, x.y, sq);
+    sq = fmaf(x.z, x.z, sq);
+    sq = fmaf(x.w, x.w, sq);
   }
-  sq = wave_sum(sq);
-  if (lane == 0) args.partials[i * args.P + E.partial_col + chunk] = sq;
+  sq = block_sum(sq, red);
+  if (threadIdx.x == 0) args.partials[i * args.P + E.partial_col + chunk] = sq;
 }
 
 // out[e] = (accumulate ? out[e] : 0) + sum_i c_i g_i[e]; examples with
@@ -269,18 +305,24 @@ __global__ __launch_bounds__(kThreads) void skinny_clip_kernel(SkClipArgs args) 
   }
 }
 
-int sk_vec(const dpsgd_layer& L) { return L.dtype == DPSGD_BF16 ? 8 : 4; }
 int64_t sk_rank(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_in : L.d_out; }
+// Narrow side rounded up to the kernel's R.
+int sk_rpad(const dpsgd_layer& L) { return sk_rank(L) <= 4 ? 4 : (sk_rank(L) <= 8 ? 8 : 16); }
+// Wide elements per lane: 16 bytes, except bf16 with R = 16 (8 bytes: 64
+// instead of 128 accumulators per lane, twice the waves per SIMD).
+int sk_vec(const dpsgd_layer& L) {
+  return L.dtype == DPSGD_BF16 ? (sk_rpad(L) == 16 ? 4 : 8) : 4;
+}
 int64_t sk_wide(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_out : L.d_in; }
 double sk_grad_bytes(const dpsgd_layer& L) { return 4.0 * (double)L.d_in * (double)L.d_out; }
 double sk_input_bytes(const dpsgd_layer& L) {
   return (double)L.T * (double)(L.d_in + L.d_out) * (L.dtype == DPSGD_BF16 ? 2.0 : 4.0);
 }
 
-template <typename TIn, int R>
+template <typename TIn, int R, int V>
 void launch_grad(const SkArgs& args, hipStream_t stream) {
   const uint32_t wgs = (args.jobs + kSkWaves - 1) / kSkWaves;
-  hipLaunchKernelGGL((skinny_grad_kernel<TIn, R>), dim3(wgs), dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((skinny_grad_kernel<TIn, R, V>), dim3(wgs), dim3(kThreads), 0, stream, args);
 }
 
 }  // namespace
@@ -315,67 +357,73 @@ size_t skinny_store_bytes(const dpsgd_layer& L, int64_t splits) {
   return round_up((size_t)splits * (size_t)L.B * (size_t)(L.d_in * L.d_out) * sizeof(float), 256);
 }
 
+// One pair of launches (grad, then finish when a layer has several row
+// ranges) per class of padded rank R and per kMaxLayersPerLaunch layers; the
+// class fixes the kernel's R and V.
 int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                         const int64_t* splits, float* const* stores, float* partials, int64_t P,
                         hipStream_t stream) {
-  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
-    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
-    SkArgs ga{}, fa{};
-    ga.n = fa.n = m;
-    ga.B = fa.B = (int32_t)layers[idx[base]].B;
-    ga.P = fa.P = P;
-    ga.partials = fa.partials = partials;
-    int64_t gjobs = 0, fjobs = 0;
-    int rmax = 0;
-    bool any_split = false;
-    for (int k = 0; k < m; ++k) {
-      const dpsgd_layer& L = layers[idx[base + k]];
-      SkEntry E{};
-      E.narrow_is_a = L.d_in <= L.d_out ? 1 : 0;
-      E.wide = E.narrow_is_a ? L.G : L.A;
-      E.narrow = E.narrow_is_a ? L.A : L.G;
-      E.store = stores[base + k];
-      E.T = (int32_t)L.T;
-      E.d_w = (int32_t)sk_wide(L);
-      E.r = (int32_t)sk_rank(L);
-      E.chunks = (int32_t)skinny_chunks(L);
-      E.splits = (int32_t)splits[base + k];
-      E.partial_col = (int32_t)cols[idx[base + k]];
-      ga.L[k] = E;
-      fa.L[k] = E;
-      ga.L[k].job_begin = (uint32_t)gjobs;
-      fa.L[k].job_begin = (uint32_t)fjobs;
-      gjobs += L.B * E.chunks * E.splits;
-      // Layers with one range are finished by the grad kernel; the finish
-      // kernel gives them no jobs (a layer with none starts where the next
-      // one does and is never the one found for a job).
-      if (E.splits > 1) {
-        fjobs += L.B * E.chunks;
-        any_split = true;
+  if (n <= 0) return DPSGD_OK;
+  const bool bf16 = layers[idx[0]].dtype == DPSGD_BF16;
+  for (int R : {4, 8, 16}) {
+    int pos[kMaxLayersPerLaunch];
+    int k0 = 0;
+    while (k0 < n) {
+      // The next up to kMaxLayersPerLaunch layers of this class.
+      int m = 0;
+      for (; k0 < n && m < kMaxLayersPerLaunch; ++k0)
+        if (sk_rpad(layers[idx[k0]]) == R) pos[m++] = k0;
+      if (m == 0) break;
+      SkArgs ga{}, fa{};
+      ga.n = fa.n = m;
+      ga.B = fa.B = (int32_t)layers[idx[0]].B;
+      ga.P = fa.P = P;
+      ga.partials = fa.partials = partials;
+      int64_t gjobs = 0, fjobs = 0;
+      for (int k = 0; k < m; ++k) {
+        const dpsgd_layer& L = layers[idx[pos[k]]];
+        SkEntry E{};
+        E.narrow_is_a = L.d_in <= L.d_out ? 1 : 0;
+        E.wide = E.narrow_is_a ? L.G : L.A;
+        E.narrow = E.narrow_is_a ? L.A : L.G;
+        E.store = stores[pos[k]];
+        E.T = (int32_t)L.T;
+        E.d_w = (int32_t)sk_wide(L);
+        E.r = (int32_t)sk_rank(L);
+        E.chunks = (int32_t)skinny_chunks(L);
+        E.splits = (int32_t)splits[pos[k]];
+        E.partial_col = (int32_t)cols[idx[pos[k]]];
+        ga.L[k] = E;
+        fa.L[k] = E;
+        ga.L[k].job_begin = (uint32_t)gjobs;
+        fa.L[k].job_begin = (uint32_t)fjobs;
+        gjobs += L.B * E.chunks * E.splits;
+        // Layers with one range are finished by the grad kernel; the finish
+        // kernel gives them no jobs (a layer with none starts where the next
+        // one does and is never the one found for a job).
+        if (E.splits > 1) fjobs += L.B * E.chunks;
       }
-      if (E.r > rmax) rmax = E.r;
-    }
-    if (gjobs > 0x7FFFFFFF || fjobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
-    ga.jobs = (uint32_t)gjobs;
-    fa.jobs = (uint32_t)fjobs;
-    const bool bf16 = layers[idx[base]].dtype == DPSGD_BF16;
-    if (bf16) {
-      if (rmax <= 4) launch_grad<uint16_t, 4>(ga, stream);
-      else if (rmax <= 8) launch_grad<uint16_t, 8>(ga, stream);
-      else launch_grad<uint16_t, 16>(ga, stream);
-    } else {
-      if (rmax <= 4) launch_grad<float, 4>(ga, stream);
-      else if (rmax <= 8) launch_grad<float, 8>(ga, stream);
-      else launch_grad<float, 16>(ga, stream);
-    }
-    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
-    if (any_split) {
-      const uint32_t wgs = (fa.jobs + kSkWaves - 1) / kSkWaves;
-      if (bf16)
-        hipLaunchKernelGGL(skinny_finish_kernel<uint16_t>, dim3(wgs), dim3(kThreads), 0, stream, fa);
-      else
-        hipLaunchKernelGGL(skinny_finish_kernel<float>, dim3(wgs), dim3(kThreads), 0, stream, fa);
+      if (gjobs > 0x7FFFFFFF || fjobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+      ga.jobs = (uint32_t)gjobs;
+      fa.jobs = (uint32_t)fjobs;
+      int V = 4;
+      if (bf16) {
+        if (R == 4) launch_grad<uint16_t, 4, 8>(ga, stream), V = 8;
+        else if (R == 8) launch_grad<uint16_t, 8, 8>(ga, stream), V = 8;
+        else launch_grad<uint16_t, 16, 4>(ga, stream);
+      } else {
+        if (R == 4) launch_grad<float, 4, 4>(ga, stream);
+        else if (R == 8) launch_grad<float, 8, 4>(ga, stream);
+        else launch_grad<float, 16, 4>(ga, stream);
+      }
       if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+      if (fjobs > 0) {
+        if (V == 8)
+          hipLaunchKernelGGL(skinny_finish_kernel<8>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
+        else
+          hipLaunchKernelGGL(skinny_finish_kernel<4>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
+        if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+      }
     }
   }
   return DPSGD_OK;
