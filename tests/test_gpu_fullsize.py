@@ -41,11 +41,14 @@ def _sample_indices(d_out, d_in, k, seed):
     return rows, cols
 
 
-@pytest.mark.parametrize("wname,n_samples", [("c3", 0), ("c4", 512), ("c5", 96)])
-def test_full_size_step(dp, wname, n_samples):
+@pytest.mark.parametrize("wname,n_samples,fused", [("c3", 0, False), ("c4", 512, False),
+                                                  ("c4", 512, True), ("c5", 96, False)])
+def test_full_size_step(dp, wname, n_samples, fused):
+    """fused: the norms and the clipped sum as one dpsgd_clipped_sum_multi call
+    (c4's rank-16 adapter pair then takes the stored per-example gradient form)."""
     import torch
     W = wl.WORKLOADS[wname]
-    _log(f"[gpu] full-size {wname}: drawing inputs")
+    _log(f"[gpu] full-size {wname} (fused={fused}): drawing inputs")
     if wname == "c3":
         hs = wl.make_layers_numpy(W)
         layers_t = []
@@ -57,12 +60,18 @@ def test_full_size_step(dp, wname, n_samples):
     else:
         layers_t = wl.make_layers_torch(W, torch.device("cuda"))
     Ls = [dp.make_layer(d["A"], d["G"], d["tensor_id"]) for d in layers_t]
-    buf = dp.alloc_step(Ls)
+    buf = dp.alloc_step(Ls, fused=fused)
     scale = 1.0 / W.B
-    # The three calls of a step; the clipped sums are copied between calls 2 and 3.
-    dp.dpsgd_per_example_norms_multi(Ls, dp.DPSGD_NORM_AUTO, buf.norms_sq, workspace=buf.norms_ws)
-    dp.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, factors_out=buf.factors,
-                                   mask_out=buf.mask, workspace=buf.clip_ws)
+    # The calls of a step; the clipped sums are copied before the noise call.
+    if fused:
+        dp.dpsgd_clipped_sum_multi(Ls, dp.DPSGD_NORM_AUTO, W.C, buf.grads, buf.norms_sq,
+                                   factors_out=buf.factors, mask_out=buf.mask,
+                                   workspace=buf.fused_ws)
+    else:
+        dp.dpsgd_per_example_norms_multi(Ls, dp.DPSGD_NORM_AUTO, buf.norms_sq,
+                                         workspace=buf.norms_ws)
+        dp.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, factors_out=buf.factors,
+                                       mask_out=buf.mask, workspace=buf.clip_ws)
     torch.cuda.synchronize()
     sums = [g.clone() for g in buf.grads]
     dp.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
