@@ -58,6 +58,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--fused", action="store_true",
+                   help="run norms + clipped sum as one dpsgd_clipped_sum_multi call (low-rank "
+                        "adapter layers read once); the norms then have no time of their own")
     p.add_argument("--cpu-sample-examples", type=int, default=4)
     p.add_argument("--pmc-probe", action="store_true",
                    help="run a 1 GiB copy and one call of each entry point, then exit "
@@ -234,7 +237,7 @@ def main():
     torch.cuda.set_device(dev)
     layers_t = wl.make_layers_torch(W, dev)
     Ls = [dpsgd.make_layer(d["A"], d["G"], d["tensor_id"]) for d in layers_t]
-    buf = dpsgd.alloc_step(Ls)
+    buf = dpsgd.alloc_step(Ls, fused=args.fused)
     forms = []
     for L in Ls:
         if L.T == 1:
@@ -272,13 +275,21 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        dpsgd.dpsgd_per_example_norms_multi(Ls, dpsgd.DPSGD_NORM_AUTO, buf.norms_sq,
-                                            workspace=buf.norms_ws)
-        if ev is not None:
-            ev[1].record()
-        dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads,
+        if args.fused:
+            # ev[1] is recorded with ev[0]: the call's time counts as the clip's.
+            if ev is not None:
+                ev[1].record()
+            dpsgd.dpsgd_clipped_sum_multi(Ls, dpsgd.DPSGD_NORM_AUTO, W.C, buf.grads, buf.norms_sq,
                                           factors_out=buf.factors, mask_out=buf.mask,
-                                          workspace=buf.clip_ws)
+                                          workspace=buf.fused_ws)
+        else:
+            dpsgd.dpsgd_per_example_norms_multi(Ls, dpsgd.DPSGD_NORM_AUTO, buf.norms_sq,
+                                                workspace=buf.norms_ws)
+            if ev is not None:
+                ev[1].record()
+            dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads,
+                                              factors_out=buf.factors, mask_out=buf.mask,
+                                              workspace=buf.clip_ws)
         if ev is not None:
             ev[2].record()
         dpsgd.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
@@ -301,13 +312,29 @@ def main():
     t_clip = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     t_noise = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
 
+    # The same step captured once as a HIP graph and replayed (no per-call
+    # launch overhead); reported beside the eager figure, not as `value`.
+    graph = dpsgd.StepGraph(Ls, buf, W.C, W.sigma, W.noise_seed, W.step, scale,
+                            dpsgd.DPSGD_NORM_AUTO, fused=args.fused)
+    for _ in range(args.warmup):
+        graph.replay()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    g0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    g1.record()
+    torch.cuda.synchronize()
+    graph_ms = g0.elapsed_time(g1) / args.steps
+    del graph
+
     t_adamw = time_noise_adamw(dpsgd, Ls, buf, W, scale, args.steps)
     adamw_gbs = work["noise_adamw_bytes"] / (t_adamw * 1e-3) / 1e9
 
     mfma_peak = PEAK_BF16_TFLOPS if W.dtype == "bf16" else PEAK_FP32_TFLOPS
     clip_tflops = work["clip_flops"] / (t_clip * 1e-3) / 1e12
-    norm_tflops = work["norm_flops"] / (t_norm * 1e-3) / 1e12
-    norm_gbs = work["input_bytes"] / (t_norm * 1e-3) / 1e9
+    norm_tflops = 0.0 if args.fused else work["norm_flops"] / (t_norm * 1e-3) / 1e12
+    norm_gbs = 0.0 if args.fused else work["input_bytes"] / (t_norm * 1e-3) / 1e9
     noise_gbs = work["noise_bytes"] / (t_noise * 1e-3) / 1e9
     value = W.B / (ms_per_step * 1e-3)
 
@@ -334,8 +361,9 @@ def main():
         "roofline": {
             "bound": "mfma",
             "kernel": (f"clip-weighted sum {dominant_kernel(W)}, timed as the whole "
-                       "dpsgd_clip_accumulate_multi call (also clip_factors_kernel and "
-                       "the split-K tail fix-up)"),
+                       + ("dpsgd_clipped_sum_multi call (the norms included)" if args.fused else
+                          "dpsgd_clip_accumulate_multi call (also clip_factors_kernel and "
+                          "the split-K tail fix-up)")),
             "achieved": clip_tflops,
             "peak": mfma_peak,
             "unit": "TFLOP/s",
@@ -343,9 +371,13 @@ def main():
             "traffic": measured_traffic(W.name),
         },
         "kernels": {
-            "norms_ms": t_norm, "norms_tflops": norm_tflops,
-            "norms_frac_mfma": norm_tflops / mfma_peak,
-            "norms_input_gbs": norm_gbs, "norms_frac_hbm": norm_gbs / PEAK_HBM_GBS,
+            "fused": args.fused,
+            "graph_ms_per_step": graph_ms,
+            "norms_ms": None if args.fused else t_norm,
+            "norms_tflops": None if args.fused else norm_tflops,
+            "norms_frac_mfma": None if args.fused else norm_tflops / mfma_peak,
+            "norms_input_gbs": None if args.fused else norm_gbs,
+            "norms_frac_hbm": None if args.fused else norm_gbs / PEAK_HBM_GBS,
             "clip_ms": t_clip, "clip_tflops": clip_tflops,
             "noise_ms": t_noise, "noise_gbs": noise_gbs, "noise_frac_hbm": noise_gbs / PEAK_HBM_GBS,
             "noise_adamw_ms": t_adamw, "noise_adamw_gbs": adamw_gbs,

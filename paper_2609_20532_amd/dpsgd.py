@@ -374,3 +374,34 @@ def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: 
                                     factors_out=buf.factors, mask_out=buf.mask,
                                     workspace=buf.clip_ws, stream=stream)
     dpsgd_add_noise_multi(layers, buf.grads, sigma, C, seed, step, scale, stream=stream)
+
+
+class StepGraph:
+    """One step captured as a HIP graph (torch.cuda.CUDAGraph) and replayed.
+
+    The library makes no allocation, memset or synchronising call while it
+    enqueues a step, so the whole step can be captured. A replay re-runs every
+    kernel with the arguments of the capture: the same input and output
+    buffers (refill the inputs in place between replays), and the same C,
+    sigma, seed, step and scale (a replay for another noise step needs a new
+    capture). It removes the per-call launch overhead, which dominates steps of
+    small layers."""
+
+    def __init__(self, layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
+                 scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, fused: bool = False):
+        import torch
+        load()
+        self._keep = (layers, buf)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):   # one eager step first, outside the capture
+            run_step(layers, buf, C, sigma, seed, step, scale, mode, fused=fused)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            run_step(layers, buf, C, sigma, seed, step, scale, mode, fused=fused)
+
+    def replay(self):
+        self.graph.replay()
+
