@@ -119,6 +119,8 @@ NORM_SHAPES = [
     (2, 256, 64, 128),     # three-tile group, full blocks
     (2, 96, 192, 64),      # one diagonal tile, ragged
     (2, 300, 64, 128),     # three row blocks: single tiles, ragged last block
+    (2, 512, 128, 64),     # four row blocks of single tiles
+    (2, 520, 64, 192),     # five row blocks, the last one 8 rows
 ]
 
 
