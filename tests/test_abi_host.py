@@ -177,3 +177,54 @@ def test_noise_adamw_rejects_null_and_misaligned_buffers(lib):
                                  None) == -1
     assert lib.dpsgd_noise_adamw(ctypes.byref(L), *good, None, -1.0, 1.0, 1, 0, 1.0,
                                  ctypes.byref(opt), None) == -1
+
+
+def _fused(lib, layers, mode=0, C=1.0, grads=(256,), norms=64, ws=512, ws_bytes=1 << 30):
+    arr = (dpsgd.dpsgd_layer * len(layers))(*layers)
+    g = (ctypes.c_void_p * len(grads))(*[ctypes.c_void_p(x) if x else None for x in grads])
+    return lib.dpsgd_clipped_sum_multi(arr, len(layers), mode, C, g, 0,
+                                       ctypes.c_void_p(norms) if norms else None, None, None,
+                                       ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), -1), (dict(T=0), -1), (dict(d_out=0), -1), (dict(A=None), -1),
+    (dict(dtype=7), -2), (dict(A=24), -1),
+])
+def test_fused_rejects_bad_layers(lib, kw, status):
+    assert _fused(lib, [_lay(**kw)]) == status
+
+
+def test_fused_rejects_bad_arguments(lib):
+    L = _lay()
+    assert _fused(lib, [L], mode=5) == -2
+    assert _fused(lib, [L], norms=None) == -1
+    assert _fused(lib, [L], grads=(None,)) == -1
+    assert _fused(lib, [L], grads=(264,)) == -1          # grad not 16-byte aligned
+    for C in (0.0, -1.0, float("nan")):
+        assert _fused(lib, [L], C=C) == -1
+    assert _fused(lib, [L], ws=None) == -3
+    assert _fused(lib, [L], ws_bytes=8) == -3
+    assert _fused(lib, [L], ws=520) == -1                # workspace not 16-byte aligned
+    assert _fused(lib, [L, _lay(B=3)], grads=(256, 512)) == -1
+
+
+def test_fused_workspace_holds_the_stored_gradients(lib):
+    """Adapter matrices (narrow side <= 16) take the stored form: the fused
+    call's workspace holds B * d_in * d_out float32 per row range for each of
+    them; with mode = GHOST it holds none and is smaller."""
+    B, T = 16, 1024
+    lora_a = dpsgd.shape_layer(B, T, 4096, 16)
+    lora_b = dpsgd.shape_layer(B, T, 16, 4096)
+    both = [lora_a, lora_b]
+    fused = dpsgd.dpsgd_clipped_sum_workspace_bytes(both)
+    ghost = dpsgd.dpsgd_clipped_sum_workspace_bytes(both, dpsgd.DPSGD_NORM_GHOST)
+    # At least one row range of per-example gradients per adapter matrix (the
+    # other workspace parts differ between the two plans).
+    assert fused >= 2 * B * 4096 * 16 * 4
+    assert fused > ghost
+    # A layer without a narrow side stores nothing: same size in both modes.
+    wide = [dpsgd.shape_layer(64, 512, 768, 3072)]
+    assert dpsgd.dpsgd_clipped_sum_workspace_bytes(wide, dpsgd.DPSGD_NORM_GHOST) == \
+        dpsgd.dpsgd_clipped_sum_workspace_bytes(wide)
+    assert dpsgd.dpsgd_clipped_sum_workspace_bytes([dpsgd.shape_layer(0, 1, 4, 4)]) == 0
