@@ -12,9 +12,9 @@
 //
 // Forming g_i: the wide side W (d_w = the larger of d_in, d_out) and the
 // narrow side n (r <= 16 columns) of an example are row-aligned, and
-// g_i = sum_t n_t (outer) W_t. One wave owns 64 V wide columns (16 bytes per
-// lane: V = 4 float32 or 8 bf16) and one range of rows, with r x V float32
-// sums per lane. Narrow values arrive 64 at a time, one per lane (lane L holds
+// g_i = sum_t n_t (outer) W_t. One wave owns 64 V wide columns (V = 4 per
+// lane: 16 bytes of float32 or 8 of bf16) and one range of rows, with r x V
+// float32 sums per lane. Narrow values arrive 64 at a time, one per lane (lane L holds
 // row L / R and column L % R of a group of 64 / R rows, R = r rounded up to 4,
 // 8 or 16), and each is broadcast to the wave with v_readlane. When the
 // examples and column chunks alone give too few waves, the rows are split into
@@ -48,7 +48,8 @@ struct SkArgs {
   uint32_t jobs;         // waves (grad kernel) or workgroups (finish kernel)
 };
 
-// V wide elements per lane and row, loaded as one 16- or 8-byte access.
+// V = 4 wide elements per lane and row, loaded as one 16-byte (float32) or
+// 8-byte (bf16) access.
 template <typename TIn, int V>
 struct SkVec;
 template <>
@@ -59,20 +60,6 @@ struct SkVec<float, 4> {
     f[1] = __uint_as_float(w.y);
     f[2] = __uint_as_float(w.z);
     f[3] = __uint_as_float(w.w);
-  }
-};
-template <>
-struct SkVec<uint16_t, 8> {
-  typedef uint4 raw;
-  __device__ static void cvt(const uint4& w, float (&f)[8]) {
-    f[0] = bf16_lo(w.x);
-    f[1] = bf16_hi(w.x);
-    f[2] = bf16_lo(w.y);
-    f[3] = bf16_hi(w.y);
-    f[4] = bf16_lo(w.z);
-    f[5] = bf16_hi(w.z);
-    f[6] = bf16_lo(w.w);
-    f[7] = bf16_hi(w.w);
   }
 };
 template <>
@@ -308,10 +295,12 @@ __global__ __launch_bounds__(kThreads) void skinny_clip_kernel(SkClipArgs args) 
 int64_t sk_rank(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_in : L.d_out; }
 // Narrow side rounded up to the kernel's R.
 int sk_rpad(const dpsgd_layer& L) { return sk_rank(L) <= 4 ? 4 : (sk_rank(L) <= 8 ? 8 : 16); }
-// Wide elements per lane: 16 bytes, except bf16 with R = 16 (8 bytes: 64
-// instead of 128 accumulators per lane, twice the waves per SIMD).
+// Wide elements per lane: four (16 bytes of float32, 8 of bf16). Chunks of
+// 256 columns divide the usual model widths (768, 2304, 4096) exactly, and
+// R x 4 accumulators leave room for four or more waves per SIMD.
 int sk_vec(const dpsgd_layer& L) {
-  return L.dtype == DPSGD_BF16 ? (sk_rpad(L) == 16 ? 4 : 8) : 4;
+  (void)L;
+  return 4;
 }
 int64_t sk_wide(const dpsgd_layer& L) { return L.d_in <= L.d_out ? L.d_out : L.d_in; }
 double sk_grad_bytes(const dpsgd_layer& L) { return 4.0 * (double)L.d_in * (double)L.d_out; }
@@ -406,10 +395,9 @@ int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const 
       if (gjobs > 0x7FFFFFFF || fjobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
       ga.jobs = (uint32_t)gjobs;
       fa.jobs = (uint32_t)fjobs;
-      int V = 4;
       if (bf16) {
-        if (R == 4) launch_grad<uint16_t, 4, 8>(ga, stream), V = 8;
-        else if (R == 8) launch_grad<uint16_t, 8, 8>(ga, stream), V = 8;
+        if (R == 4) launch_grad<uint16_t, 4, 4>(ga, stream);
+        else if (R == 8) launch_grad<uint16_t, 8, 4>(ga, stream);
         else launch_grad<uint16_t, 16, 4>(ga, stream);
       } else {
         if (R == 4) launch_grad<float, 4, 4>(ga, stream);
@@ -418,10 +406,7 @@ int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const 
       }
       if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
       if (fjobs > 0) {
-        if (V == 8)
-          hipLaunchKernelGGL(skinny_finish_kernel<8>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
-        else
-          hipLaunchKernelGGL(skinny_finish_kernel<4>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
+        hipLaunchKernelGGL(skinny_finish_kernel<4>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
         if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
       }
     }

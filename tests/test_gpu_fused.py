@@ -59,7 +59,7 @@ SETS = [
     # stored layers together with layers of every other kernel family
     (4, wl.BF16, [(256, 768, 8), (256, 256, 384), (256, 256, 256), (256, 8, 768), (256, 40, 24)]),
     (6, wl.F32, [(64, 512, 2), (64, 96, 80), (64, 2, 512), (1, 256, 128)]),
-    # bf16 rank 12 (8-byte lanes): a wide side of 100, not a multiple of 8
+    # bf16 rank 12: a wide side of 100 (25 four-element lanes of one chunk)
     (3, wl.BF16, [(200, 100, 12), (200, 12, 100)]),
 ]
 
@@ -101,7 +101,7 @@ def _stored(L):
     whole number of the kernel's per-lane vectors, gradient <= 1/4 of the
     input bytes)."""
     r, w = min(L.d_in, L.d_out), max(L.d_in, L.d_out)
-    vec = (8 if r <= 8 else 4) if L.dtype == wl.BF16 else 4
+    vec = 4
     esz = 2 if L.dtype == wl.BF16 else 4
     return r <= 16 and w % vec == 0 and 16 * L.d_in * L.d_out <= L.T * (L.d_in + L.d_out) * esz
 
