@@ -61,7 +61,7 @@ def parse():
     p.add_argument("--fused", action="store_true",
                    help="run norms + clipped sum as one dpsgd_clipped_sum_multi call (low-rank "
                         "adapter layers read once); the norms then have no time of their own")
-    p.add_argument("--cpu-sample-examples", type=int, default=24)
+    p.add_argument("--cpu-sample-examples", type=int, default=40)
     p.add_argument("--pmc-probe", action="store_true",
                    help="run a 1 GiB copy and one call of each entry point, then exit "
                         "(for rocprofv3 counter passes)")
