@@ -29,7 +29,12 @@
  *    once the caller synchronises with the stream. Faults inside a kernel
  *    surface at that synchronisation.
  *  - Every entry point returns a dpsgd_status. Nothing aborts or throws across
- *    the ABI. On an error return nothing has been enqueued.
+ *    the ABI. An error found by the argument checks returns before anything
+ *    is enqueued. DPSGD_ERR_HIP (a launch the runtime rejected) and
+ *    DPSGD_ERR_INVALID_ARG for a grid too large for one launch (beyond 2^31
+ *    workgroups, far past any size the checks accept in practice) can come
+ *    after earlier kernels of the same call were enqueued; the outputs are
+ *    then unspecified.
  *  - Results are deterministic: the same inputs on the same device give
  *    bitwise-identical outputs (no floating-point atomics).
  *  - Arithmetic: products of bf16 inputs are exact in float32 and all sums
