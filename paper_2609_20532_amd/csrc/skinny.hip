@@ -14,11 +14,12 @@
 // narrow side n (r <= 16 columns) of an example are row-aligned, and
 // g_i = sum_t n_t (outer) W_t. One wave owns 64 V wide columns (V = 4 per
 // lane: 16 bytes of float32 or 8 of bf16) and one range of rows, with r x V
-// float32 sums per lane. Narrow values arrive 64 at a time, one per lane (lane L holds
-// row L / R and column L % R of a group of 64 / R rows, R = r rounded up to 4,
-// 8 or 16), and each is broadcast to the wave with v_readlane. When the
-// examples and column chunks alone give too few waves, the rows are split into
-// ranges whose partial gradients a second kernel adds in range order.
+// float32 sums per lane, and takes 16 rows per iteration (16 wide loads in
+// flight per lane). Narrow values arrive 64 at a time, one per lane (lane L
+// holds row L / R and column L % R of a group of 64 / R rows, R = r rounded
+// up to 4, 8 or 16), and each is broadcast to the wave with v_readlane. When
+// the examples and column chunks alone give too few waves, the rows are split
+// into ranges whose partial gradients a second kernel adds in range order.
 #include "common.h"
 
 namespace dpsgd {
@@ -91,6 +92,8 @@ template <typename TIn, int R, int V>
 __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
   typedef typename SkVec<TIn, V>::raw Raw;
   constexpr int G = 64 / R;   // rows per narrow load
+  constexpr int U = 16 / G > 1 ? 16 / G : 1;   // narrow loads per iteration
+  constexpr int RI = G * U;   // rows per iteration: 16 wide loads in flight per lane
   const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
   if (job >= args.jobs) return;   // whole waves
   const int lane = threadIdx.x & 63;
@@ -114,24 +117,30 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
 #pragma unroll
     for (int v = 0; v < V; ++v) acc[j][v] = 0.f;
 
-  for (int tg = t0; tg < t1; tg += G) {
-    const int rows = min(G, t1 - tg);   // wave-uniform
-    float nv = 0.f;
-    if (ncol < E.r && nrow < rows) nv = sk_load(Nr + (int64_t)(tg + nrow) * E.r + ncol);
-    Raw wv[G];
+  for (int tg = t0; tg < t1; tg += RI) {
+    const int rows = min(RI, t1 - tg);   // wave-uniform
+    float nv[U];
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
+    for (int uu = 0; uu < U; ++uu) {
+      nv[uu] = 0.f;
+      if (ncol < E.r && uu * G + nrow < rows)
+        nv[uu] = sk_load(Nr + (int64_t)(tg + uu * G + nrow) * E.r + ncol);
+    }
+    Raw wv[RI];
+#pragma unroll
+    for (int u = 0; u < RI; ++u) {
       wv[u] = Raw{};
       if (u < rows && col_ok) wv[u] = *reinterpret_cast<const Raw*>(W + (int64_t)(tg + u) * E.d_w);
     }
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
+    for (int u = 0; u < RI; ++u) {
       if (u < rows) {   // wave-uniform
         float f[V];
         SkVec<TIn, V>::cvt(wv[u], f);
 #pragma unroll
         for (int j = 0; j < R; ++j) {
-          const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(nv), u * R + j));
+          const float a = __int_as_float(
+              __builtin_amdgcn_readlane(__float_as_int(nv[u / G]), (u % G) * R + j));
 #pragma unroll
           for (int v = 0; v < V; ++v) acc[j][v] = fmaf(a, f[v], acc[j][v]);
         }
