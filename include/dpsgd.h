@@ -161,11 +161,12 @@ int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
  * the same results as dpsgd_per_example_norms_multi(..., accumulate = 0)
  * followed by dpsgd_clip_accumulate_multi, within float32 rounding. A layer
  * whose narrow side min(d_in, d_out) is at most 16 (a low-rank adapter
- * matrix), whose wide side is a multiple of 16 bytes and whose per-example
- * gradient (4 d_in d_out bytes) is at most a quarter of its per-example input
- * bytes (T (d_in + d_out) element bytes) is read once: every G_i^T A_i is
- * formed in float32 and stored in the workspace, its squared norm is summed
- * from the stored values and the clipped sum is formed from them. Other layers
+ * matrix), whose wide side is a multiple of 4 elements (at most 2^30) and
+ * whose per-example gradient (4 d_in d_out bytes) is at most a quarter of its
+ * per-example input bytes (T (d_in + d_out) element bytes) is read once:
+ * every G_i^T A_i is formed in float32 and stored in the workspace, its
+ * squared norm is summed from the stored values and the clipped sum is
+ * formed from them. Other layers
  * use the kernels of the separate calls. mode applies to the other layers;
  * DPSGD_NORM_GHOST also turns the stored form off. workspace: at least
  * dpsgd_clipped_sum_workspace_bytes(layers, n_layers, mode) bytes (device,

@@ -327,7 +327,8 @@ void launch_grad(const SkArgs& args, hipStream_t stream) {
 
 bool skinny_ok(const dpsgd_layer& L) {
   if (sk_rank(L) > kSkinnyMaxRank) return false;
-  if (sk_wide(L) % sk_vec(L) != 0) return false;
+  // Lane column indices are 32-bit: keep the wide side well inside int32.
+  if (sk_wide(L) % sk_vec(L) != 0 || sk_wide(L) > (INT64_C(1) << 30)) return false;
   // The stored gradients must be much smaller than the inputs they replace.
   return 4.0 * sk_grad_bytes(L) <= sk_input_bytes(L);
 }
