@@ -18,7 +18,7 @@ from oracle import philox
 from paper_2609_20532_amd import workloads as wl
 
 from parity_util import (TOL, assert_sum_close, device_layers, guard_band, oracle_layers,
-                         rel_err, to_device, torch_to_float64)
+                         rel_err, torch_to_float64)
 
 pytestmark = pytest.mark.gpu
 
