@@ -296,11 +296,11 @@ def main():
         if ev is not None:
             ev[3].record()
 
+    # The events exist before the warm-up, so nothing but the required
+    # synchronisation separates the warm-up from the timed steps.
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
