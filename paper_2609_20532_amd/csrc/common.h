@@ -106,6 +106,15 @@ int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int
                      float* partials, int64_t P, hipStream_t stream);
 
 bool tr_tile_ok(const dpsgd_layer& L);
+// k-major float32 kernel (gemm.hip): float32, T a multiple of 32, d_in and d_out
+// multiples of 4 and at most 2^24. Tiles are 64 x 256 for d_out <= 64, else
+// 128 x 128 (rows along d_out, columns along d_in).
+bool k32_ok(const dpsgd_layer& L);
+int k32_tile_m(const dpsgd_layer& L);
+int k32_tile_n(const dpsgd_layer& L);
+// Output tiles of the materialised-norm kernel that takes the layer (one norm
+// partial per tile and example).
+int64_t mat_tile_count(const dpsgd_layer& L);
 int64_t tr_q_total(const dpsgd_layer& L);
 int tr_cu_count();
 

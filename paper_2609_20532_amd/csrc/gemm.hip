@@ -27,6 +27,7 @@
 // Split K. Small outputs are split along K to fill the GPU; each split writes
 // its own fp32 partial and a second kernel adds them in split order, so the
 // result is deterministic.
+#include "lds_dma.h"
 #include "mma.h"
 
 namespace dpsgd {
@@ -314,6 +315,232 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_kernel(TGemmArgs args) {
   }
 }
 
+// ------------------------------------------- float32, k-major slices in LDS
+//
+// Float32 layers with T % 32 == 0 and both widths multiples of 4. A 32-row
+// slice of both operands is copied to LDS unchanged, row-major [k][cols], by
+// direct 16-byte global-to-LDS copies. v_mfma_f32_32x32x2f32 takes lane l's
+// operand at row (first operand) or column (second) l % 32 and k = l / 32, so
+// one wave reads 32 consecutive words of rows k and k + 1 per operand block:
+// no transpose anywhere. Odd rows are stored rotated by 32 columns, so the two
+// half-waves (rows k and k + 1, same columns) hit different LDS banks.
+// The tile is 128 x 128 (2 x 2 waves) or, for d_out <= 64, 64 x 256 (1 x 4
+// waves), so a narrow G side does not leave half of every tile empty; each
+// wave owns 64 x 64 as 2 x 2 blocks of 32 x 32. Two slice buffers of up to
+// 40 KB let two workgroups share a CU. Clip weights are applied on the
+// accumulator (T % 32 == 0 makes every step lie inside one example); an
+// example whose factor is 0 is neither copied nor multiplied.
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kK32Rows = 32;                                  // k rows per slice
+constexpr int kK32StageFloats = kK32Rows * (64 + 256);        // largest slice (64 x 256 tile)
+constexpr int kK32MaxCopies = kK32StageFloats / 256 / 4;      // 1 KB copies per wave (10)
+
+struct K32Entry {
+  const float* Xm;       // G: [B*T][M]
+  const float* Xn;       // A: [B*T][N]
+  float* out;            // EPI_STORE: grad (splits == 1) or this layer's split partials
+  int32_t M, N, T;
+  int32_t tm;            // tile rows (along M): 64 or 128
+  int32_t tn;            // tile columns (along N): 256 or 128
+  int32_t tiles_n;
+  int32_t splits, q_per_split;
+  uint32_t wg_begin;
+  int32_t partial_col;   // EPI_SUMSQ
+  int32_t accumulate;    // EPI_STORE, splits == 1
+  int32_t pad;
+};
+
+struct K32Args {
+  K32Entry L[kMaxLayersPerLaunch];
+  int32_t n;
+  int32_t B;
+  const float* factors;
+  float* partials;
+  int64_t P;
+};
+
+template <int SCALE, int EPI>
+__global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
+  __shared__ __attribute__((aligned(16))) float lds[2 * kK32StageFloats];
+
+  int l = 0;
+  {
+    int lo = 0, hi = args.n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (args.L[mid].wg_begin <= blockIdx.x) lo = mid; else hi = mid - 1;
+    }
+    l = lo;
+  }
+  const K32Entry& E = args.L[l];
+  const int TM = E.tm, TN = E.tn;
+  const int tiles_mn = ((E.M + TM - 1) / TM) * E.tiles_n;
+  // Within a layer, consecutive jobs (the tiles of one K range) run on one XCD
+  // and share its L2. All jobs of a layer cost the same, while layers differ
+  // (a layer's K range per job can be 32 times another's), so every XCD takes
+  // an equal share of each layer rather than a contiguous part of the grid.
+  const uint32_t n_l = (uint32_t)tiles_mn * (uint32_t)(EPI == EPI_SUMSQ ? args.B : E.splits);
+  const uint32_t w = xcd_two_class_index(blockIdx.x - E.wg_begin, n_l, n_l);
+  const int outer = (int)(w / (uint32_t)tiles_mn);  // split (STORE) or example (SUMSQ)
+  const int tile = (int)(w % (uint32_t)tiles_mn);
+  const int tmi = tile / E.tiles_n, tni = tile % E.tiles_n;
+
+  const int spe = E.T / kK32Rows;
+  int64_t q0, q1;
+  if (EPI == EPI_SUMSQ) {
+    q0 = (int64_t)outer * spe;
+    q1 = q0 + spe;
+  } else {
+    q0 = (int64_t)outer * E.q_per_split;
+    q1 = min(q0 + (int64_t)E.q_per_split, (int64_t)args.B * spe);
+  }
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wc = TN / 64;
+  const int wm = wave / wc, wn = wave % wc;
+  const int h = lane >> 5, c32 = lane & 31;
+
+  // Clip factors through the scalar cache (constant address space), so they
+  // never count against vmcnt, which tracks the slice copies.
+  typedef __attribute__((address_space(4))) const float const_float;
+  const const_float* fac = (const const_float*)args.factors;
+
+  // Copy p of this wave moves 1 KB chunk c = wave + 4 p of the slice: chunks
+  // [0, TM / 8) hold the G rows (TM columns each), the rest the A rows (TN
+  // columns). Lane i writes words 4 i .. 4 i + 3 of its chunk; the source
+  // column undoes the odd-row rotation and is clamped into the row (columns
+  // past the edge feed only outputs that are never stored).
+  const int nm = TM / 8, ncopy = (TM + TN) / 8;   // 1 KB chunks: G side, whole slice
+  uint32_t voff[kK32MaxCopies];
+#pragma unroll
+  for (int p = 0; p < kK32MaxCopies; ++p) {
+    const int c = wave + 4 * p;
+    const bool mside = c < nm;
+    const int W = mside ? TM : TN, R = mside ? E.M : E.N;
+    const int f = 256 * (mside ? c : c - nm) + 4 * lane;
+    const int k = f / W, pc = f & (W - 1);
+    const int col = ((mside ? tmi * TM : tni * TN) + ((pc + W - 32 * (k & 1)) & (W - 1)));
+    voff[p] = (uint32_t)k * (uint32_t)R * 4u + (uint32_t)min(col, R - 4) * 4u;
+  }
+  const uint32_t lds0 = lds_address(lds);
+  const char* Gb = reinterpret_cast<const char*>(E.Xm);
+  const char* Ab = reinterpret_cast<const char*>(E.Xn);
+  const int64_t gslice = (int64_t)kK32Rows * E.M * 4, aslice = (int64_t)kK32Rows * E.N * 4;
+
+  auto issue = [&](int64_t qq, int slot) {
+    if (SCALE == SCALE_ACC && fac[(int)(qq / spe)] == 0.0f) return;
+    const char* gs = Gb + qq * gslice;
+    const char* as = Ab + qq * aslice;
+    const uint32_t dst = lds0 + (uint32_t)slot * (kK32StageFloats * 4);
+#pragma unroll
+    for (int p = 0; p < kK32MaxCopies; ++p) {
+      const int c = wave + 4 * p;
+      if (c < ncopy) copy16_to_lds(c < nm ? gs : as, voff[p], dst + 1024u * (uint32_t)c);
+    }
+  };
+
+  // Operand words of this lane: row k = 2 kp + h of block a (G side) or b (A side).
+  int offa[2], offb[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    offa[a] = h * TM + ((wm * 64 + 32 * a + 32 * h) & (TM - 1)) + c32;
+    offb[a] = kK32Rows * TM + h * TN + ((wn * 64 + 32 * a + 32 * h) & (TN - 1)) + c32;
+  }
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+  float c_cur = 1.0f;    // accumulator unit (SCALE_ACC): acc * c_cur is the weighted sum
+  bool started = false;
+
+  if (q0 < q1) issue(q0, 0);
+  for (int64_t q = q0; q < q1; ++q) {
+    // Slice q is complete for this wave once nothing is outstanding; the
+    // barrier makes every wave's copies visible and guarantees that slice
+    // q - 1, whose buffer is refilled next, is no longer read.
+    wait_vmcnt<0>();
+    barrier_no_wait();
+    if (q + 1 < q1) issue(q + 1, (int)((q + 1 - q0) & 1));
+    bool skip = false;
+    if (SCALE == SCALE_ACC) {
+      const float c_new = fac[(int)(q / spe)];
+      skip = c_new == 0.0f;
+      if (!skip) {
+        if (started && c_cur != c_new) {
+          const float sc = c_cur / c_new;
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) acc[a][b] *= sc;
+        }
+        c_cur = c_new;
+        started = true;
+      }
+    }
+    if (skip) continue;
+    const float* S = lds + (int)((q - q0) & 1) * kK32StageFloats;
+    const float* pa0 = S + offa[0];
+    const float* pa1 = S + offa[1];
+    const float* pb0 = S + offb[0];
+    const float* pb1 = S + offb[1];
+#pragma unroll
+    for (int kp = 0; kp < kK32Rows / 2; ++kp) {
+      const float a0 = pa0[2 * kp * TM], a1 = pa1[2 * kp * TM];
+      const float b0 = pb0[2 * kp * TN], b1 = pb1[2 * kp * TN];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+    }
+  }
+
+  // Output v of block (a, b) in this lane: row 8 (v / 4) + 4 h + v % 4 and
+  // column l % 32 of the block.
+  const int m_base = tmi * TM + wm * 64, n_base = tni * TN + wn * 64;
+  if (EPI == EPI_SUMSQ) {
+    float s = 0.f;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const bool nok = n_base + 32 * b + c32 < E.N;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = m_base + 32 * a + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (nok && m < E.M) s = fmaf(acc[a][b][v], acc[a][b][v], s);
+        }
+      }
+    __syncthreads();   // the slice buffers are free: reuse them for the reduction
+    s = block_sum(s, lds);
+    if (threadIdx.x == 0) args.partials[(int64_t)outer * args.P + E.partial_col + tile] = s;
+  } else {
+    float* out = E.out + (E.splits > 1 ? (int64_t)outer * E.M * E.N : 0);
+    const bool add = E.splits == 1 && E.accumulate;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int n = n_base + 32 * b + c32;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = m_base + 32 * a + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (m < E.M && n < E.N) {
+            float* p = out + (int64_t)m * E.N + n;
+            const float r = SCALE == SCALE_ACC ? acc[a][b][v] * c_cur : acc[a][b][v];
+            *p = add ? *p + r : r;
+          }
+        }
+      }
+  }
+}
+
 // --------------------------------------------------------- split-K reduce
 
 struct SplitEntry {
@@ -330,8 +557,12 @@ struct SplitArgs {
   int32_t n;
 };
 
-constexpr int kSplitElemsPerWG = kThreads * 4 * 4;  // 4 float4 per thread
+constexpr int kSplitElemsPerWG = kThreads * 4;  // one float4 per thread
 
+// Adds the partials in split order. A layer can have tens of splits, so the
+// loads of eight consecutive splits are issued before their adds (the order
+// of the additions does not change) and each thread owns one float4, which
+// gives enough workgroups to cover the GPU.
 __global__ __launch_bounds__(kThreads) void split_reduce_kernel(SplitArgs args) {
   int lo = 0, hi = args.n - 1;
   while (lo < hi) {
@@ -339,25 +570,31 @@ __global__ __launch_bounds__(kThreads) void split_reduce_kernel(SplitArgs args) 
     if (args.L[mid].wg_begin <= blockIdx.x) lo = mid; else hi = mid - 1;
   }
   const SplitEntry& E = args.L[lo];
-  const int64_t base = (int64_t)(blockIdx.x - E.wg_begin) * kSplitElemsPerWG;
+  const int64_t e = (int64_t)(blockIdx.x - E.wg_begin) * kSplitElemsPerWG + (int64_t)threadIdx.x * 4;
+  if (e >= E.numel) return;
+  const int S = E.splits;
+  if (E.vec) {
+    float4 v = E.accumulate ? *reinterpret_cast<const float4*>(E.grad + e)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float* part = E.part + e;
+    int s = 0;
+    for (; s + 8 <= S; s += 8) {
+      float4 p[8];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int64_t e = base + ((int64_t)u * kThreads + threadIdx.x) * 4;
-    if (e >= E.numel) break;
-    if (E.vec) {
-      float4 v = E.accumulate ? *reinterpret_cast<const float4*>(E.grad + e)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int s = 0; s < E.splits; ++s) {
-        const float4 p = *reinterpret_cast<const float4*>(E.part + (int64_t)s * E.numel + e);
-        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-      }
-      *reinterpret_cast<float4*>(E.grad + e) = v;
-    } else {
-      for (int k = 0; k < 4 && e + k < E.numel; ++k) {
-        float v = E.accumulate ? E.grad[e + k] : 0.f;
-        for (int s = 0; s < E.splits; ++s) v += E.part[(int64_t)s * E.numel + e + k];
-        E.grad[e + k] = v;
-      }
+      for (int u = 0; u < 8; ++u) p[u] = *reinterpret_cast<const float4*>(part + (int64_t)(s + u) * E.numel);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) { v.x += p[u].x; v.y += p[u].y; v.z += p[u].z; v.w += p[u].w; }
+    }
+    for (; s < S; ++s) {
+      const float4 p = *reinterpret_cast<const float4*>(part + (int64_t)s * E.numel);
+      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    *reinterpret_cast<float4*>(E.grad + e) = v;
+  } else {
+    for (int k = 0; k < 4 && e + k < E.numel; ++k) {
+      float v = E.accumulate ? E.grad[e + k] : 0.f;
+      for (int s = 0; s < S; ++s) v += E.part[(int64_t)s * E.numel + e + k];
+      E.grad[e + k] = v;
     }
   }
 }
@@ -426,7 +663,67 @@ int launch_tgemm_group(const dpsgd_layer* layers, const int* idx, int n, const f
   return DPSGD_OK;
 }
 
+template <int SCALE, int EPI>
+int launch_k32_group(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
+                     float* const* outs, const int* splits, const int* accumulate,
+                     const int64_t* cols, float* partials, int64_t P, hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    K32Args args{};
+    args.n = m;
+    args.B = (int32_t)layers[idx[base]].B;
+    args.factors = factors;
+    args.partials = partials;
+    args.P = P;
+    int64_t wgs = 0;
+    for (int k = 0; k < m; ++k) {
+      const int li = idx[base + k];
+      const dpsgd_layer& L = layers[li];
+      K32Entry& E = args.L[k];
+      E.Xm = static_cast<const float*>(L.G);
+      E.Xn = static_cast<const float*>(L.A);
+      E.M = (int32_t)L.d_out;
+      E.N = (int32_t)L.d_in;
+      E.T = (int32_t)L.T;
+      E.tm = k32_tile_m(L);
+      E.tn = k32_tile_n(L);
+      E.tiles_n = (int32_t)ceil_div(L.d_in, E.tn);
+      const int64_t tiles = ceil_div(L.d_out, E.tm) * E.tiles_n;
+      E.wg_begin = (uint32_t)wgs;
+      if (EPI == EPI_STORE) {
+        E.out = outs[base + k];
+        E.splits = splits[base + k];
+        E.q_per_split = (int32_t)ceil_div(L.B * (L.T / kK32Rows), E.splits);
+        E.accumulate = accumulate ? accumulate[base + k] : 0;
+        wgs += tiles * E.splits;
+      } else {
+        E.partial_col = (int32_t)cols[li];
+        wgs += tiles * L.B;
+      }
+    }
+    if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL((tgemm_k32_kernel<SCALE, EPI>), dim3((uint32_t)wgs), dim3(kThreads), 0,
+                       stream, args);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
+}
+
 }  // namespace
+
+bool k32_ok(const dpsgd_layer& L) {
+  // The copies address a slice with 32-bit per-lane offsets: 32 rows of d * 4
+  // bytes must stay below 2^32.
+  return L.dtype == DPSGD_F32 && L.T % kK32Rows == 0 && L.d_in % 4 == 0 && L.d_out % 4 == 0 &&
+         L.d_in <= (INT64_C(1) << 24) && L.d_out <= (INT64_C(1) << 24);
+}
+int k32_tile_m(const dpsgd_layer& L) { return L.d_out <= 64 ? 64 : 128; }
+int k32_tile_n(const dpsgd_layer& L) { return L.d_out <= 64 ? 256 : 128; }
+int64_t mat_tile_count(const dpsgd_layer& L) {
+  if (tr_tile_ok(L)) return (L.d_out / 256) * (L.d_in / 256);
+  if (k32_ok(L)) return ceil_div(L.d_out, k32_tile_m(L)) * ceil_div(L.d_in, k32_tile_n(L));
+  return ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+}
 
 void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // Layers on the 256- and 384x256-tile kernels are balanced by their own
@@ -442,8 +739,10 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // its own.
   const int cus = tr_cu_count();
   int tr_idx[kMaxLayersPerLaunch], n_tr = 0, wd_idx[kMaxLayersPerLaunch], n_wd = 0;
-  int64_t work[4] = {0, 0, 0, 0};   // output tiles x K steps per 128-tile launch
+  // output tiles x K steps per launch: 128-tile variants 0..3, k-major float32 4
+  int64_t work[5] = {0, 0, 0, 0, 0};
   auto group = [](const dpsgd_layer& L) {
+    if (k32_ok(L)) return 4;
     const bool vec = L.dtype == DPSGD_BF16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     return (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
   };
@@ -451,8 +750,7 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
     const dpsgd_layer& L = layers[l];
     if (wide_tile_ok(L)) wd_idx[n_wd++] = l;
     else if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
-    else work[group(L)] += ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile) *
-                           clip_q_total(L, clip_scale_mode(L));
+    else work[group(L)] += mat_tile_count(L) * clip_q_total(L, clip_scale_mode(L));
   }
   constexpr int64_t kMinStepsPerSplit = 4;
   constexpr int64_t kMaxSplits = 1024;
@@ -486,16 +784,17 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
                     hipStream_t stream) {
   // Group layers by kernel variant; each group is one grouped launch.
   const bool bf16 = layers[0].dtype == DPSGD_BF16;
-  int idx[6][kMaxLayersPerLaunch];
-  float* outs[6][kMaxLayersPerLaunch];
-  int spl[6][kMaxLayersPerLaunch];
-  int acc[6][kMaxLayersPerLaunch];
-  int cnt[6] = {0, 0, 0, 0, 0, 0};
+  int idx[7][kMaxLayersPerLaunch];
+  float* outs[7][kMaxLayersPerLaunch];
+  int spl[7][kMaxLayersPerLaunch];
+  int acc[7][kMaxLayersPerLaunch];
+  int cnt[7] = {0, 0, 0, 0, 0, 0, 0};
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     const int g = wide_tile_ok(L) ? 5
                   : tr_tile_ok(L) ? 4
+                  : k32_ok(L)     ? 6
                                   : (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
     const int k = cnt[g]++;
     idx[g][k] = l;
@@ -533,6 +832,9 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
     DPSGD_TG(float, false, SCALE_OPERAND, 3);
   }
 #undef DPSGD_TG
+  if (st == DPSGD_OK && cnt[6])
+    st = launch_k32_group<SCALE_ACC, EPI_STORE>(layers, idx[6], cnt[6], factors, outs[6], spl[6],
+                                                acc[6], nullptr, nullptr, 0, stream);
   if (st != DPSGD_OK) return st;
 
   // Split-K fix-up for the layers that were split.
@@ -562,16 +864,20 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
 int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream) {
   const bool bf16 = layers[idx[0]].dtype == DPSGD_BF16;
-  int iv[256], is[256], ib[256], nv = 0, ns = 0, nb = 0;
+  int iv[256], is[256], ib[256], ik[256], nv = 0, ns = 0, nb = 0, nk = 0;
   for (int k = 0; k < n; ++k) {
     const dpsgd_layer& L = layers[idx[k]];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     if (tr_tile_ok(L)) ib[nb++] = idx[k];
+    else if (k32_ok(L)) ik[nk++] = idx[k];
     else if (vec) iv[nv++] = idx[k];
     else is[ns++] = idx[k];
   }
   int st = DPSGD_OK;
   if (nb) st = launch_tr_mat_norms(layers, ib, nb, cols, partials, P, stream);
+  if (st == DPSGD_OK && nk)
+    st = launch_k32_group<SCALE_NONE, EPI_SUMSQ>(layers, ik, nk, nullptr, nullptr, nullptr, nullptr,
+                                                 cols, partials, P, stream);
   if (st != DPSGD_OK) return st;
   if (bf16) {
     if (nv) st = launch_tgemm_group<uint16_t, true, SCALE_NONE, EPI_SUMSQ>(

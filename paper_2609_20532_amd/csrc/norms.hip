@@ -347,8 +347,9 @@ NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode) {
   const int64_t nt = ceil_div(L.T, kTile);
   const double ghost = (double)(nt * (nt + 1) / 2) *
                        (double)(ceil_div(L.d_in, bk) * bk + ceil_div(L.d_out, bk) * bk);
-  const double mat = (double)(ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile)) *
-                     (double)(ceil_div(L.T, bk) * bk);
+  // (A k-major float32 tile, 64 x 256 or 128 x 128, has the area of a 128 x 128 one.)
+  const int64_t mt = k32_ok(L) ? mat_tile_count(L) : ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+  const double mat = (double)mt * (double)(ceil_div(L.T, bk) * bk);
   return ghost <= mat ? FORM_GHOST : FORM_MAT;
 }
 
@@ -361,8 +362,7 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
       return nt * (nt + 1) / 2;
     }
     default:
-      if (tr_tile_ok(L)) return (L.d_out / 256) * (L.d_in / 256);
-      return ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
+      return mat_tile_count(L);
   }
 }
 

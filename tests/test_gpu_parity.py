@@ -121,6 +121,8 @@ NORM_SHAPES = [
     (2, 300, 64, 128),     # three row blocks: single tiles, ragged last block
     (2, 512, 128, 64),     # four row blocks of single tiles
     (2, 520, 64, 192),     # five row blocks, the last one 8 rows
+    (3, 64, 520, 60),      # float32 k-major kernel, 64 x 256 tiles, ragged in both widths
+    (2, 96, 132, 260),     # float32 k-major kernel, 128 x 128 tiles, ragged in both widths
 ]
 
 
@@ -213,6 +215,8 @@ CLIP_SHAPES = [
     (3, 9, 11, 7, wl.F32),
     (4, 64, 96, 80, wl.F32),        # float32, T a multiple of the K step: weight on the accumulator
     (3, 32, 27, 10, wl.F32),        # the same with element loads (widths not multiples of 4)
+    (6, 96, 520, 60, wl.F32),       # float32 k-major kernel: 64 x 256 tiles, ragged, split along K
+    (5, 128, 132, 260, wl.F32),     # float32 k-major kernel: 128 x 128 tiles, ragged
     (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
     (8, 256, 256, 256, wl.BF16),    # 256x256-tile kernel, split along K
     (4, 64, 256, 384, wl.BF16),     # 384x256-tile kernel, one tile split along K
@@ -220,6 +224,7 @@ CLIP_SHAPES = [
     (8, 256, 256, 384, wl.BF16),    # 384x256-tile kernel, d_out not a multiple of 256, long K
 ]
 TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-5:]
+K32_NARROW, K32_SQUARE = CLIP_SHAPES[-7:-5]
 
 
 def _weights_in_fp32(shape):
@@ -270,7 +275,7 @@ def test_clip_sum_matches_oracle(dp, shape):
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[2], TILE256_ONE_SPLIT, TILE256_SPLIT_K,
-                                   WIDE_ONE_TILE, WIDE_FOUR_TILES])
+                                   WIDE_ONE_TILE, WIDE_FOUR_TILES, K32_NARROW, K32_SQUARE])
 def test_zero_factor_examples_contribute_nothing(dp, shape):
     """An example whose squared norm is +inf gets factor C/inf = 0; with finite
     inputs its clipped gradient 0 * g_i is exactly zero (Section 2.2)."""
@@ -297,7 +302,7 @@ def test_zero_factor_examples_contribute_nothing(dp, shape):
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[1], CLIP_SHAPES[2], CLIP_SHAPES[4], TILE256_ONE_SPLIT,
-                                   WIDE_FOUR_TILES])
+                                   WIDE_FOUR_TILES, K32_NARROW])
 def test_zero_factor_example_with_nonfinite_inputs_contributes_nothing(dp, shape):
     """Reading: an example whose factor is 0 adds nothing to the sum, even when
     its activations and gradients hold inf or NaN (its rows are not used)."""
@@ -333,7 +338,8 @@ def test_zero_factor_example_with_nonfinite_inputs_contributes_nothing(dp, shape
     assert_sum_close(got, ref, TOL[dtype], "clipped sum without the zero-factor example")
 
 
-@pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2], TILE256_SPLIT_K, WIDE_ONE_TILE])
+@pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2], TILE256_SPLIT_K, WIDE_ONE_TILE,
+                                   K32_SQUARE])
 def test_clip_sum_accumulates(dp, shape):
     h, got, ref, *_ = _clip_case(dp, shape, 1.0, accumulate=True)
     assert_sum_close(got, ref, TOL[shape[4]], "accumulated clipped sum")
