@@ -217,4 +217,5 @@ if __name__ == "__main__":
     import sys
 
     args = dict(a.split("=", 1) for a in sys.argv[1:])
-    print(json.dumps(bench(B=int(args.get("B", 512)))), flush=True)
+    print(json.dumps(bench(B=int(args.get("B", 512)), steps=int(args.get("steps", 5)),
+                           warmup=int(args.get("warmup", 2)))), flush=True)

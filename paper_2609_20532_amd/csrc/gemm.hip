@@ -734,9 +734,9 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   // few output tiles but a long K range would otherwise run on a handful of
   // CUs.
   // The balance is per launch: layers of different kernel instances (vector
-  // or element loads, weight on the accumulator or on the operand) run in
-  // separate launches, one after the other, so each launch fills the GPU on
-  // its own.
+  // or element loads, weight on the accumulator or on the operand, k-major
+  // float32) run in separate launches, one after the other, so each launch
+  // fills the GPU on its own.
   const int cus = tr_cu_count();
   int tr_idx[kMaxLayersPerLaunch], n_tr = 0, wd_idx[kMaxLayersPerLaunch], n_wd = 0;
   // output tiles x K steps per launch: 128-tile variants 0..3, k-major float32 4
@@ -754,20 +754,63 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   }
   constexpr int64_t kMinStepsPerSplit = 4;
   constexpr int64_t kMaxSplits = 1024;
-  const int64_t target = 4 * (int64_t)cus;   // workgroups per launch
+  auto split_count = [](int64_t q_total, int64_t chunk) {
+    int64_t s = ceil_div(q_total, chunk);
+    if (s > q_total / kMinStepsPerSplit) s = q_total / kMinStepsPerSplit;
+    if (s > kMaxSplits) s = kMaxSplits;
+    return s < 1 ? (int64_t)1 : s;
+  };
+  // Both kernels hold two workgroups per CU. A launch runs in rounds of that
+  // many workgroups, and a round that is only partly filled costs as much as
+  // a full one, so the chunk (K steps per workgroup) is chosen per launch:
+  // for r = 1 .. 8 rounds, the smallest chunk whose workgroups fit r rounds,
+  // keeping the r with the least r x (longest workgroup in K steps).
+  const int64_t slots = 2 * (int64_t)cus;
+  int64_t chunk_of[5] = {1, 1, 1, 1, 1};
+  for (int g = 0; g < 5; ++g) {
+    if (work[g] == 0) continue;
+    int64_t q_max = 1;
+    for (int l = 0; l < n_layers; ++l)
+      if (!wide_tile_ok(layers[l]) && !tr_tile_ok(layers[l]) && group(layers[l]) == g) {
+        const int64_t q = clip_q_total(layers[l], clip_scale_mode(layers[l]));
+        if (q > q_max) q_max = q;
+      }
+    // Workgroups of the launch and its longest K range, for a given chunk.
+    auto eval = [&](int64_t chunk, int64_t* longest) {
+      int64_t wgs = 0, lg = 0;
+      for (int l = 0; l < n_layers; ++l) {
+        const dpsgd_layer& L = layers[l];
+        if (wide_tile_ok(L) || tr_tile_ok(L) || group(L) != g) continue;
+        const int64_t q = clip_q_total(L, clip_scale_mode(L));
+        const int64_t sp = split_count(q, chunk);
+        wgs += mat_tile_count(L) * sp;
+        const int64_t len = ceil_div(q, sp);
+        if (len > lg) lg = len;
+      }
+      if (longest) *longest = lg;
+      return wgs;
+    };
+    int64_t best_chunk = q_max, best_cost = -1;
+    for (int64_t r = 1; r <= 8; ++r) {
+      if (eval(q_max, nullptr) > r * slots) continue;   // not even one split per layer fits
+      int64_t lo = kMinStepsPerSplit < q_max ? kMinStepsPerSplit : q_max, hi = q_max;
+      while (lo < hi) {   // smallest chunk with at most r rounds of workgroups
+        const int64_t mid = (lo + hi) / 2;
+        if (eval(mid, nullptr) <= r * slots) hi = mid; else lo = mid + 1;
+      }
+      int64_t longest = 0;
+      eval(lo, &longest);
+      const int64_t cost = r * longest;
+      if (best_cost < 0 || cost < best_cost) { best_cost = cost; best_chunk = lo; }
+    }
+    chunk_of[g] = best_chunk;
+  }
   size_t off = 0;
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     int64_t s = 1;
-    if (!wide_tile_ok(L) && !tr_tile_ok(L)) {
-      const int64_t q_total = clip_q_total(L, clip_scale_mode(L));
-      int64_t chunk = ceil_div(work[group(L)], target);
-      if (chunk < kMinStepsPerSplit) chunk = kMinStepsPerSplit;
-      s = ceil_div(q_total, chunk);
-      if (s > q_total / kMinStepsPerSplit) s = q_total / kMinStepsPerSplit;
-      if (s > kMaxSplits) s = kMaxSplits;
-      if (s < 1) s = 1;
-    }
+    if (!wide_tile_ok(L) && !tr_tile_ok(L))
+      s = split_count(clip_q_total(L, clip_scale_mode(L)), chunk_of[group(L)]);
     plan->splits[l] = (int)s;
     plan->partial_offset[l] = off;
     if (s > 1) off += round_up((size_t)s * (size_t)L.d_out * (size_t)L.d_in * sizeof(float), 256);
