@@ -112,6 +112,11 @@ bool tr_tile_ok(const dpsgd_layer& L);
 bool k32_ok(const dpsgd_layer& L);
 int k32_tile_m(const dpsgd_layer& L);
 int k32_tile_n(const dpsgd_layer& L);
+// Layers whose g_i has at most 512 entries (gemm.hip) form g_i on the VALU:
+// one norm partial per example; the clip runs tiny_jobs(L) jobs of
+// consecutive examples, one partial sum each.
+bool tiny_ok(const dpsgd_layer& L);
+int tiny_jobs(const dpsgd_layer& L);
 // Output tiles of the materialised-norm kernel that takes the layer (one norm
 // partial per tile and example).
 int64_t mat_tile_count(const dpsgd_layer& L);

@@ -663,6 +663,156 @@ int launch_tgemm_group(const dpsgd_layer* layers, const int* idx, int n, const f
   return DPSGD_OK;
 }
 
+// ------------------------------------------------------ tiny layers (VALU)
+//
+// Layers with at most kTinyMaxOut entries in g_i = G_i^T A_i (a stem
+// convolution's 16 x 27, a small head) would leave an MFMA tile almost empty,
+// so each example's gradient is formed directly: its rows are staged in LDS a
+// chunk at a time and thread t accumulates entries t and t + 256 of g_i in
+// float32. The norm variant sums g_i's squares per example; the clip variant
+// adds c_i g_i to the job's partial sum (an example with c_i = 0 is skipped,
+// its rows are never read).
+
+constexpr int kTinyMaxOut = 2 * kThreads;     // d_in * d_out
+constexpr int kTinyLdsFloats = 16384;         // 64 KB of staged rows
+constexpr int kTinyBatch = 16;                // loads in flight per thread while staging
+
+struct TinyEntry {
+  const void* A;          // [B*T][N]
+  const void* G;          // [B*T][M]
+  float* out;             // EPI_STORE: grad (one job) or this layer's per-job partials
+  int32_t M, N, T;
+  int32_t ex_per_job;
+  int32_t jobs;
+  uint32_t wg_begin;
+  int32_t partial_col;    // EPI_SUMSQ
+  int32_t accumulate;     // EPI_STORE, jobs == 1
+};
+
+struct TinyArgs {
+  TinyEntry L[kMaxLayersPerLaunch];
+  int32_t n;
+  int32_t B;
+  const float* factors;
+  float* partials;
+  int64_t P;
+};
+
+template <typename TIn, int EPI>
+__global__ __launch_bounds__(kThreads) void tiny_kernel(TinyArgs args) {
+  __shared__ float rows[kTinyLdsFloats];
+  __shared__ float red[4];
+  int lo = 0, hi = args.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.L[mid].wg_begin <= blockIdx.x) lo = mid; else hi = mid - 1;
+  }
+  const TinyEntry& E = args.L[lo];
+  const int job = (int)(blockIdx.x - E.wg_begin);
+  const int M = E.M, N = E.N, T = E.T, W = M + N;
+  const int rc = kTinyLdsFloats / W;   // rows per chunk
+  const TIn* A = static_cast<const TIn*>(E.A);
+  const TIn* G = static_cast<const TIn*>(E.G);
+  const int tid = threadIdx.x;
+  const int n_out = M * N;
+  const int o0 = tid, o1 = tid + kThreads;
+  const int m0 = o0 / N, n0 = o0 - m0 * N, m1 = o1 / N, n1 = o1 - m1 * N;
+  float sum0 = 0.f, sum1 = 0.f;   // EPI_STORE: sum over this job's examples of c_i g_i
+  const int ex_begin = job * E.ex_per_job;
+  const int ex_end = min(ex_begin + E.ex_per_job, args.B);
+  for (int ex = ex_begin; ex < ex_end; ++ex) {
+    const float c = EPI == EPI_STORE ? args.factors[ex] : 1.0f;
+    if (EPI == EPI_STORE && c == 0.0f) continue;   // uniform over the workgroup
+    float g0 = 0.f, g1 = 0.f;
+    for (int r0 = 0; r0 < T; r0 += rc) {
+      const int nr = min(rc, T - r0);
+      const int64_t row = (int64_t)ex * T + r0;
+      // Staged chunk: rows [r][0, M) hold G, [r][M, M + N) hold A.
+      __syncthreads();   // the previous chunk is no longer read
+      // kTinyBatch independent loads per thread, then their LDS stores, so the
+      // staging waits for one memory latency per batch rather than per element.
+      const int n_el = nr * W;
+      for (int i0 = 0; i0 < n_el; i0 += kThreads * kTinyBatch) {
+        float v[kTinyBatch];
+#pragma unroll
+        for (int u = 0; u < kTinyBatch; ++u) {
+          const int i = i0 + u * kThreads + tid;
+          v[u] = 0.f;
+          if (i < n_el) {
+            const int r = i / W, k = i - r * W;
+            v[u] = k < M ? load_elem(G + (row + r) * M + k) : load_elem(A + (row + r) * N + (k - M));
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kTinyBatch; ++u) {
+          const int i = i0 + u * kThreads + tid;
+          if (i < n_el) rows[i] = v[u];
+        }
+      }
+      __syncthreads();
+      if (o0 < n_out)
+        for (int r = 0; r < nr; ++r) g0 = fmaf(rows[r * W + m0], rows[r * W + M + n0], g0);
+      if (o1 < n_out)
+        for (int r = 0; r < nr; ++r) g1 = fmaf(rows[r * W + m1], rows[r * W + M + n1], g1);
+    }
+    if (EPI == EPI_SUMSQ) {
+      const float s = block_sum(g0 * g0 + g1 * g1, red);
+      if (tid == 0) args.partials[(int64_t)ex * args.P + E.partial_col] = s;
+    } else {
+      sum0 = fmaf(c, g0, sum0);
+      sum1 = fmaf(c, g1, sum1);
+    }
+  }
+  if (EPI == EPI_STORE) {
+    float* out = E.out + (E.jobs > 1 ? (int64_t)job * n_out : 0);
+    const bool add = E.jobs == 1 && E.accumulate;
+    if (o0 < n_out) out[o0] = add ? out[o0] + sum0 : sum0;
+    if (o1 < n_out) out[o1] = add ? out[o1] + sum1 : sum1;
+  }
+}
+
+template <typename TIn, int EPI>
+int launch_tiny_group(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
+                      float* const* outs, const int* jobs, const int* accumulate,
+                      const int64_t* cols, float* partials, int64_t P, hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    TinyArgs args{};
+    args.n = m;
+    args.B = (int32_t)layers[idx[base]].B;
+    args.factors = factors;
+    args.partials = partials;
+    args.P = P;
+    int64_t wgs = 0;
+    for (int k = 0; k < m; ++k) {
+      const int li = idx[base + k];
+      const dpsgd_layer& L = layers[li];
+      TinyEntry& E = args.L[k];
+      E.A = L.A;
+      E.G = L.G;
+      E.M = (int32_t)L.d_out;
+      E.N = (int32_t)L.d_in;
+      E.T = (int32_t)L.T;
+      E.wg_begin = (uint32_t)wgs;
+      if (EPI == EPI_STORE) {
+        E.out = outs[base + k];
+        E.jobs = jobs[base + k];
+        E.accumulate = accumulate ? accumulate[base + k] : 0;
+      } else {
+        E.jobs = (int32_t)L.B;
+        E.partial_col = (int32_t)cols[li];
+      }
+      // A job past the last example writes zeros, so the count may overshoot.
+      E.ex_per_job = (int32_t)ceil_div(L.B, E.jobs);
+      wgs += E.jobs;
+    }
+    if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    hipLaunchKernelGGL((tiny_kernel<TIn, EPI>), dim3((uint32_t)wgs), dim3(kThreads), 0, stream, args);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
+}
+
 template <int SCALE, int EPI>
 int launch_k32_group(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
                      float* const* outs, const int* splits, const int* accumulate,
@@ -719,6 +869,12 @@ bool k32_ok(const dpsgd_layer& L) {
 }
 int k32_tile_m(const dpsgd_layer& L) { return L.d_out <= 64 ? 64 : 128; }
 int k32_tile_n(const dpsgd_layer& L) { return L.d_out <= 64 ? 256 : 128; }
+bool tiny_ok(const dpsgd_layer& L) { return L.d_in * L.d_out <= kTinyMaxOut; }
+int tiny_jobs(const dpsgd_layer& L) {
+  // About two workgroups per CU, each over ceil(B / jobs) consecutive examples.
+  const int64_t want = L.B < 2 * (int64_t)tr_cu_count() ? L.B : 2 * (int64_t)tr_cu_count();
+  return (int)ceil_div(L.B, ceil_div(L.B, want));
+}
 int64_t mat_tile_count(const dpsgd_layer& L) {
   if (tr_tile_ok(L)) return (L.d_out / 256) * (L.d_in / 256);
   if (k32_ok(L)) return ceil_div(L.d_out, k32_tile_m(L)) * ceil_div(L.d_in, k32_tile_n(L));
@@ -746,11 +902,13 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
     const bool vec = L.dtype == DPSGD_BF16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     return (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
   };
+  // Layers on the 128-tile and k-major kernels (the others have their own plans).
+  auto split_k = [](const dpsgd_layer& L) { return !wide_tile_ok(L) && !tr_tile_ok(L) && !tiny_ok(L); };
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     if (wide_tile_ok(L)) wd_idx[n_wd++] = l;
     else if (tr_tile_ok(L)) tr_idx[n_tr++] = l;
-    else work[group(L)] += mat_tile_count(L) * clip_q_total(L, clip_scale_mode(L));
+    else if (split_k(L)) work[group(L)] += mat_tile_count(L) * clip_q_total(L, clip_scale_mode(L));
   }
   constexpr int64_t kMinStepsPerSplit = 4;
   constexpr int64_t kMaxSplits = 1024;
@@ -771,7 +929,7 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
     if (work[g] == 0) continue;
     int64_t q_max = 1;
     for (int l = 0; l < n_layers; ++l)
-      if (!wide_tile_ok(layers[l]) && !tr_tile_ok(layers[l]) && group(layers[l]) == g) {
+      if (split_k(layers[l]) && group(layers[l]) == g) {
         const int64_t q = clip_q_total(layers[l], clip_scale_mode(layers[l]));
         if (q > q_max) q_max = q;
       }
@@ -780,7 +938,7 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
       int64_t wgs = 0, lg = 0;
       for (int l = 0; l < n_layers; ++l) {
         const dpsgd_layer& L = layers[l];
-        if (wide_tile_ok(L) || tr_tile_ok(L) || group(L) != g) continue;
+        if (!split_k(L) || group(L) != g) continue;
         const int64_t q = clip_q_total(L, clip_scale_mode(L));
         const int64_t sp = split_count(q, chunk);
         wgs += mat_tile_count(L) * sp;
@@ -809,8 +967,8 @@ void plan_clip(const dpsgd_layer* layers, int n_layers, ClipPlan* plan) {
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     int64_t s = 1;
-    if (!wide_tile_ok(L) && !tr_tile_ok(L))
-      s = split_count(clip_q_total(L, clip_scale_mode(L)), chunk_of[group(L)]);
+    if (split_k(L)) s = split_count(clip_q_total(L, clip_scale_mode(L)), chunk_of[group(L)]);
+    else if (tiny_ok(L)) s = tiny_jobs(L);   // one partial per job of consecutive examples
     plan->splits[l] = (int)s;
     plan->partial_offset[l] = off;
     if (s > 1) off += round_up((size_t)s * (size_t)L.d_out * (size_t)L.d_in * sizeof(float), 256);
@@ -827,16 +985,17 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
                     hipStream_t stream) {
   // Group layers by kernel variant; each group is one grouped launch.
   const bool bf16 = layers[0].dtype == DPSGD_BF16;
-  int idx[7][kMaxLayersPerLaunch];
-  float* outs[7][kMaxLayersPerLaunch];
-  int spl[7][kMaxLayersPerLaunch];
-  int acc[7][kMaxLayersPerLaunch];
-  int cnt[7] = {0, 0, 0, 0, 0, 0, 0};
+  int idx[8][kMaxLayersPerLaunch];
+  float* outs[8][kMaxLayersPerLaunch];
+  int spl[8][kMaxLayersPerLaunch];
+  int acc[8][kMaxLayersPerLaunch];
+  int cnt[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   for (int l = 0; l < n_layers; ++l) {
     const dpsgd_layer& L = layers[l];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     const int g = wide_tile_ok(L) ? 5
                   : tr_tile_ok(L) ? 4
+                  : tiny_ok(L)    ? 7
                   : k32_ok(L)     ? 6
                                   : (vec ? 0 : 1) + (clip_scale_mode(L) == SCALE_ACC ? 0 : 2);
     const int k = cnt[g]++;
@@ -878,6 +1037,11 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
   if (st == DPSGD_OK && cnt[6])
     st = launch_k32_group<SCALE_ACC, EPI_STORE>(layers, idx[6], cnt[6], factors, outs[6], spl[6],
                                                 acc[6], nullptr, nullptr, 0, stream);
+  if (st == DPSGD_OK && cnt[7])
+    st = bf16 ? launch_tiny_group<uint16_t, EPI_STORE>(layers, idx[7], cnt[7], factors, outs[7], spl[7],
+                                                       acc[7], nullptr, nullptr, 0, stream)
+              : launch_tiny_group<float, EPI_STORE>(layers, idx[7], cnt[7], factors, outs[7], spl[7],
+                                                    acc[7], nullptr, nullptr, 0, stream);
   if (st != DPSGD_OK) return st;
 
   // Split-K fix-up for the layers that were split.
@@ -907,11 +1071,12 @@ int launch_clip_sum(const dpsgd_layer* layers, int n_layers, const float* factor
 int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream) {
   const bool bf16 = layers[idx[0]].dtype == DPSGD_BF16;
-  int iv[256], is[256], ib[256], ik[256], nv = 0, ns = 0, nb = 0, nk = 0;
+  int iv[256], is[256], ib[256], ik[256], it[256], nv = 0, ns = 0, nb = 0, nk = 0, nt = 0;
   for (int k = 0; k < n; ++k) {
     const dpsgd_layer& L = layers[idx[k]];
     const bool vec = bf16 ? tgemm_vec_ok<uint16_t>(L) : tgemm_vec_ok<float>(L);
     if (tr_tile_ok(L)) ib[nb++] = idx[k];
+    else if (tiny_ok(L)) it[nt++] = idx[k];
     else if (k32_ok(L)) ik[nk++] = idx[k];
     else if (vec) iv[nv++] = idx[k];
     else is[ns++] = idx[k];
@@ -921,6 +1086,11 @@ int launch_mat_norms(const dpsgd_layer* layers, const int* idx, int n, const int
   if (st == DPSGD_OK && nk)
     st = launch_k32_group<SCALE_NONE, EPI_SUMSQ>(layers, ik, nk, nullptr, nullptr, nullptr, nullptr,
                                                  cols, partials, P, stream);
+  if (st == DPSGD_OK && nt)
+    st = bf16 ? launch_tiny_group<uint16_t, EPI_SUMSQ>(layers, it, nt, nullptr, nullptr, nullptr,
+                                                       nullptr, cols, partials, P, stream)
+              : launch_tiny_group<float, EPI_SUMSQ>(layers, it, nt, nullptr, nullptr, nullptr, nullptr,
+                                                    cols, partials, P, stream);
   if (st != DPSGD_OK) return st;
   if (bf16) {
     if (nv) st = launch_tgemm_group<uint16_t, true, SCALE_NONE, EPI_SUMSQ>(

@@ -362,7 +362,7 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
       return nt * (nt + 1) / 2;
     }
     default:
-      return mat_tile_count(L);
+      return tiny_ok(L) ? 1 : mat_tile_count(L);
   }
 }
 

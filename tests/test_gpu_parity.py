@@ -123,6 +123,7 @@ NORM_SHAPES = [
     (2, 520, 64, 192),     # five row blocks, the last one 8 rows
     (3, 64, 520, 60),      # float32 k-major kernel, 64 x 256 tiles, ragged in both widths
     (2, 96, 132, 260),     # float32 k-major kernel, 128 x 128 tiles, ragged in both widths
+    (5, 64, 27, 16),       # stem-convolution widths: g_i formed on the VALU
 ]
 
 
@@ -215,6 +216,10 @@ CLIP_SHAPES = [
     (3, 9, 11, 7, wl.F32),
     (4, 64, 96, 80, wl.F32),        # float32, T a multiple of the K step: weight on the accumulator
     (3, 32, 27, 10, wl.F32),        # the same with element loads (widths not multiples of 4)
+    (3, 40, 30, 25, wl.F32),        # transposing kernel, element loads (g_i above the VALU path's 512)
+    (4, 70, 26, 21, wl.BF16),       # the same for bfloat16
+    (1100, 8, 27, 16, wl.F32),      # VALU path, jobs of 3 consecutive examples
+    (1, 40, 8, 8, wl.F32),          # VALU path, a single job writing the gradient directly
     (6, 96, 520, 60, wl.F32),       # float32 k-major kernel: 64 x 256 tiles, ragged, split along K
     (5, 128, 132, 260, wl.F32),     # float32 k-major kernel: 128 x 128 tiles, ragged
     (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
@@ -225,6 +230,8 @@ CLIP_SHAPES = [
 ]
 TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-5:]
 K32_NARROW, K32_SQUARE = CLIP_SHAPES[-7:-5]
+TINY_JOBS, TINY_ONE_JOB = CLIP_SHAPES[-9:-7]
+TINY_BF16 = CLIP_SHAPES[5]
 
 
 def _weights_in_fp32(shape):
@@ -275,7 +282,8 @@ def test_clip_sum_matches_oracle(dp, shape):
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[2], TILE256_ONE_SPLIT, TILE256_SPLIT_K,
-                                   WIDE_ONE_TILE, WIDE_FOUR_TILES, K32_NARROW, K32_SQUARE])
+                                   WIDE_ONE_TILE, WIDE_FOUR_TILES, K32_NARROW, K32_SQUARE, TINY_JOBS,
+                                   TINY_BF16])
 def test_zero_factor_examples_contribute_nothing(dp, shape):
     """An example whose squared norm is +inf gets factor C/inf = 0; with finite
     inputs its clipped gradient 0 * g_i is exactly zero (Section 2.2)."""
@@ -302,7 +310,7 @@ def test_zero_factor_examples_contribute_nothing(dp, shape):
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[1], CLIP_SHAPES[2], CLIP_SHAPES[4], TILE256_ONE_SPLIT,
-                                   WIDE_FOUR_TILES, K32_NARROW])
+                                   WIDE_FOUR_TILES, K32_NARROW, TINY_JOBS, TINY_BF16])
 def test_zero_factor_example_with_nonfinite_inputs_contributes_nothing(dp, shape):
     """Reading: an example whose factor is 0 adds nothing to the sum, even when
     its activations and gradients hold inf or NaN (its rows are not used)."""
@@ -339,7 +347,7 @@ def test_zero_factor_example_with_nonfinite_inputs_contributes_nothing(dp, shape
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[0], CLIP_SHAPES[2], TILE256_SPLIT_K, WIDE_ONE_TILE,
-                                   K32_SQUARE])
+                                   K32_SQUARE, TINY_JOBS, TINY_ONE_JOB])
 def test_clip_sum_accumulates(dp, shape):
     h, got, ref, *_ = _clip_case(dp, shape, 1.0, accumulate=True)
     assert_sum_close(got, ref, TOL[shape[4]], "accumulated clipped sum")
