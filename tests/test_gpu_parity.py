@@ -220,6 +220,7 @@ CLIP_SHAPES = [
     (4, 70, 26, 21, wl.BF16),       # the same for bfloat16
     (1100, 8, 27, 16, wl.F32),      # VALU path, jobs of 3 consecutive examples
     (1, 40, 8, 8, wl.F32),          # VALU path, a single job writing the gradient directly
+    (40, 1, 16, 10, wl.F32),        # VALU path, T = 1 (a classifier head)
     (6, 96, 520, 60, wl.F32),       # float32 k-major kernel: 64 x 256 tiles, ragged, split along K
     (5, 128, 132, 260, wl.F32),     # float32 k-major kernel: 128 x 128 tiles, ragged
     (4, 64, 256, 512, wl.BF16),     # 256x256-tile kernel, one split
@@ -230,7 +231,7 @@ CLIP_SHAPES = [
 ]
 TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-5:]
 K32_NARROW, K32_SQUARE = CLIP_SHAPES[-7:-5]
-TINY_JOBS, TINY_ONE_JOB = CLIP_SHAPES[-9:-7]
+TINY_JOBS, TINY_ONE_JOB = CLIP_SHAPES[-10:-8]
 TINY_BF16 = CLIP_SHAPES[5]
 
 
