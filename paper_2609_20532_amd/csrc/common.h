@@ -112,6 +112,7 @@ bool tr_tile_ok(const dpsgd_layer& L);
 bool k32_ok(const dpsgd_layer& L);
 int k32_tile_m(const dpsgd_layer& L);
 int k32_tile_n(const dpsgd_layer& L);
+int k32_ex_per_job(const dpsgd_layer& L);   // examples per materialised-norm job
 // Layers whose g_i has at most 512 entries (gemm.hip) form g_i on the VALU:
 // one norm partial per example; the clip runs tiny_jobs(L) jobs of
 // consecutive examples, one partial sum each.

@@ -349,7 +349,7 @@ struct K32Entry {
   uint32_t wg_begin;
   int32_t partial_col;   // EPI_SUMSQ
   int32_t accumulate;    // EPI_STORE, splits == 1
-  int32_t pad;
+  int32_t ex_per_job;    // EPI_SUMSQ: consecutive examples of one job
 };
 
 struct K32Args {
@@ -381,17 +381,21 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   // and share its L2. All jobs of a layer cost the same, while layers differ
   // (a layer's K range per job can be 32 times another's), so every XCD takes
   // an equal share of each layer rather than a contiguous part of the grid.
-  const uint32_t n_l = (uint32_t)tiles_mn * (uint32_t)(EPI == EPI_SUMSQ ? args.B : E.splits);
+  const int n_outer = EPI == EPI_SUMSQ ? (args.B + E.ex_per_job - 1) / E.ex_per_job : E.splits;
+  const uint32_t n_l = (uint32_t)tiles_mn * (uint32_t)n_outer;
   const uint32_t w = xcd_two_class_index(blockIdx.x - E.wg_begin, n_l, n_l);
-  const int outer = (int)(w / (uint32_t)tiles_mn);  // split (STORE) or example (SUMSQ)
+  const int outer = (int)(w / (uint32_t)tiles_mn);  // split (STORE) or example group (SUMSQ)
   const int tile = (int)(w % (uint32_t)tiles_mn);
   const int tmi = tile / E.tiles_n, tni = tile % E.tiles_n;
 
   const int spe = E.T / kK32Rows;
   int64_t q0, q1;
   if (EPI == EPI_SUMSQ) {
-    q0 = (int64_t)outer * spe;
-    q1 = q0 + spe;
+    // A job runs the copy pipeline across ex_per_job consecutive examples of
+    // one tile, so a short T does not leave the workgroup mostly in its
+    // prologue and epilogue.
+    q0 = (int64_t)outer * E.ex_per_job * spe;
+    q1 = (int64_t)min((outer + 1) * E.ex_per_job, args.B) * spe;
   } else {
     q0 = (int64_t)outer * E.q_per_split;
     q1 = min(q0 + (int64_t)E.q_per_split, (int64_t)args.B * spe);
@@ -460,12 +464,19 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   float c_cur = 1.0f;    // accumulator unit (SCALE_ACC): acc * c_cur is the weighted sum
   bool started = false;
 
+  // Output v of block (a, b) in this lane: row 8 (v / 4) + 4 h + v % 4 and
+  // column l % 32 of the block.
+  const int m_base = tmi * TM + wm * 64, n_base = tni * TN + wn * 64;
+  bool stored = false;   // EPI_SUMSQ: a partial was stored after the last copies
+
   if (q0 < q1) issue(q0, 0);
   for (int64_t q = q0; q < q1; ++q) {
-    // Slice q is complete for this wave once nothing is outstanding; the
-    // barrier makes every wave's copies visible and guarantees that slice
-    // q - 1, whose buffer is refilled next, is no longer read.
-    wait_vmcnt<0>();
+    // Slice q is complete for this wave once nothing is outstanding but the
+    // partial stored after its copies were issued (loads and stores complete
+    // in order); the barrier makes every wave's copies visible and guarantees
+    // that slice q - 1, whose buffer is refilled next, is no longer read.
+    if (EPI == EPI_SUMSQ && stored) wait_vmcnt<1>();
+    else wait_vmcnt<0>();
     barrier_no_wait();
     if (q + 1 < q1) issue(q + 1, (int)((q + 1 - q0) & 1));
     bool skip = false;
@@ -499,28 +510,31 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
       acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
       acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
     }
+    stored = false;
+    if (EPI == EPI_SUMSQ && (q + 1) % spe == 0) {
+      // End of an example: this wave's share of ||G_i^T A_i||_F^2 over the
+      // tile (rows and columns past the edges masked), one partial per wave.
+      float s = 0.f;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const bool nok = n_base + 32 * b + c32 < E.N;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int m = m_base + 32 * a + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (nok && m < E.M) s = fmaf(acc[a][b][v], acc[a][b][v], s);
+            acc[a][b][v] = 0.0f;
+          }
+        }
+      s = wave_sum(s);
+      if (lane == 0)
+        args.partials[(q / spe) * args.P + E.partial_col + 4 * tile + wave] = s;
+      stored = true;
+    }
   }
 
-  // Output v of block (a, b) in this lane: row 8 (v / 4) + 4 h + v % 4 and
-  // column l % 32 of the block.
-  const int m_base = tmi * TM + wm * 64, n_base = tni * TN + wn * 64;
-  if (EPI == EPI_SUMSQ) {
-    float s = 0.f;
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const bool nok = n_base + 32 * b + c32 < E.N;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int m = m_base + 32 * a + 8 * (v >> 2) + 4 * h + (v & 3);
-          if (nok && m < E.M) s = fmaf(acc[a][b][v], acc[a][b][v], s);
-        }
-      }
-    __syncthreads();   // the slice buffers are free: reuse them for the reduction
-    s = block_sum(s, lds);
-    if (threadIdx.x == 0) args.partials[(int64_t)outer * args.P + E.partial_col + tile] = s;
-  } else {
+  if (EPI == EPI_STORE) {
     float* out = E.out + (E.splits > 1 ? (int64_t)outer * E.M * E.N : 0);
     const bool add = E.splits == 1 && E.accumulate;
 #pragma unroll
@@ -848,7 +862,8 @@ int launch_k32_group(const dpsgd_layer* layers, const int* idx, int n, const flo
         wgs += tiles * E.splits;
       } else {
         E.partial_col = (int32_t)cols[li];
-        wgs += tiles * L.B;
+        E.ex_per_job = k32_ex_per_job(L);
+        wgs += tiles * ceil_div(L.B, E.ex_per_job);
       }
     }
     if (wgs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
@@ -869,6 +884,11 @@ bool k32_ok(const dpsgd_layer& L) {
 }
 int k32_tile_m(const dpsgd_layer& L) { return L.d_out <= 64 ? 64 : 128; }
 int k32_tile_n(const dpsgd_layer& L) { return L.d_out <= 64 ? 256 : 128; }
+int k32_ex_per_job(const dpsgd_layer& L) {
+  // About 16 K steps (512 rows) per materialised-norm job, at most 8 examples.
+  const int64_t e = 16 / (L.T / kK32Rows);
+  return (int)(e < 1 ? 1 : e > 8 ? 8 : e);
+}
 bool tiny_ok(const dpsgd_layer& L) { return L.d_in * L.d_out <= kTinyMaxOut; }
 int tiny_jobs(const dpsgd_layer& L) {
   // About two workgroups per CU, each over ceil(B / jobs) consecutive examples.

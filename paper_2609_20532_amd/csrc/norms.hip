@@ -361,8 +361,8 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
       const int64_t nt = ceil_div(L.T, kTile);
       return nt * (nt + 1) / 2;
     }
-    default:
-      return tiny_ok(L) ? 1 : mat_tile_count(L);
+    default:   // the k-major float32 kernel writes one partial per wave of a tile
+      return tiny_ok(L) ? 1 : k32_ok(L) ? 4 * mat_tile_count(L) : mat_tile_count(L);
   }
 }
 
