@@ -419,6 +419,7 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   // past the edge feed only outputs that are never stored).
   const int nm = TM / 8, ncopy = (TM + TN) / 8;   // 1 KB chunks: G side, whole slice
   uint32_t voff[kK32MaxCopies];
+  uint32_t inside = 0;   // bit p: copy p's columns lie inside the row
 #pragma unroll
   for (int p = 0; p < kK32MaxCopies; ++p) {
     const int c = wave + 4 * p;
@@ -428,6 +429,7 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
     const int k = f / W, pc = f & (W - 1);
     const int col = ((mside ? tmi * TM : tni * TN) + ((pc + W - 32 * (k & 1)) & (W - 1)));
     voff[p] = (uint32_t)k * (uint32_t)R * 4u + (uint32_t)min(col, R - 4) * 4u;
+    if (col < R) inside |= 1u << p;
   }
   const uint32_t lds0 = lds_address(lds);
   const char* Gb = reinterpret_cast<const char*>(E.Xm);
@@ -442,7 +444,13 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
 #pragma unroll
     for (int p = 0; p < kK32MaxCopies; ++p) {
       const int c = wave + 4 * p;
-      if (c < ncopy) copy16_to_lds(c < nm ? gs : as, voff[p], dst + 1024u * (uint32_t)c);
+      // For the norms, a lane whose columns lie past the edge copies nothing:
+      // its LDS words keep the zeros written at the start, so rows and
+      // columns outside the tile's valid part contribute exactly 0.
+      // (The LDS address is made wave-uniform before the per-lane branch.)
+      const uint32_t la = __builtin_amdgcn_readfirstlane(dst + 1024u * (uint32_t)c);
+      if (c < ncopy && (EPI != EPI_SUMSQ || ((inside >> p) & 1u)))
+        copy16_to_lds(c < nm ? gs : as, voff[p], la);
     }
   };
 
@@ -469,6 +477,12 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   const int m_base = tmi * TM + wm * 64, n_base = tni * TN + wn * 64;
   bool stored = false;   // EPI_SUMSQ: a partial was stored after the last copies
 
+  if (EPI == EPI_SUMSQ && ((tmi + 1) * TM > E.M || (tni + 1) * TN > E.N)) {
+    // Edge tile: clear both slice buffers once (see issue()).
+    for (int i = threadIdx.x * 4; i < 2 * kK32StageFloats; i += kThreads * 4)
+      *reinterpret_cast<float4*>(lds + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+  }
   if (q0 < q1) issue(q0, 0);
   for (int64_t q = q0; q < q1; ++q) {
     // Slice q is complete for this wave once nothing is outstanding but the
@@ -513,20 +527,17 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
     stored = false;
     if (EPI == EPI_SUMSQ && (q + 1) % spe == 0) {
       // End of an example: this wave's share of ||G_i^T A_i||_F^2 over the
-      // tile (rows and columns past the edges masked), one partial per wave.
+      // tile (entries past the edges are exactly 0), one partial per wave.
       float s = 0.f;
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          const bool nok = n_base + 32 * b + c32 < E.N;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int m = m_base + 32 * a + 8 * (v >> 2) + 4 * h + (v & 3);
-            if (nok && m < E.M) s = fmaf(acc[a][b][v], acc[a][b][v], s);
+            s = fmaf(acc[a][b][v], acc[a][b][v], s);
             acc[a][b][v] = 0.0f;
           }
-        }
       s = wave_sum(s);
       if (lane == 0)
         args.partials[(q / spe) * args.P + E.partial_col + 4 * tile + wave] = s;
