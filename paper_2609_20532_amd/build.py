@@ -24,7 +24,7 @@ LIB = os.path.join(PKG, "libdpsgd.so")
 VERIFIER_LIB = os.path.join(PKG, "libdpsgd_verifier.so")
 VERIFIER_SOURCES = ["verifier.cpp"]
 OBJ_DIR = os.path.join(PKG, "_build")
-SOURCES = ["api.hip", "noise.hip", "norms.hip", "ghost.hip", "gemm.hip", "gemm_tr.hip", "gemm_wide.hip",
+SOURCES = ["api.hip", "noise.hip", "norms.hip", "ghost.hip", "gram32.hip", "gemm.hip", "gemm_tr.hip", "gemm_wide.hip",
            "skinny.hip"]
 ARCH = "gfx950"
 

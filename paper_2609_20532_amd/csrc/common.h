@@ -102,6 +102,11 @@ int launch_skinny_clip(const dpsgd_layer* layers, const int* idx, int n, float* 
 // multiples of 256, T a multiple of 32), K slices of a layer, launchers.
 // Gram-form norms with direct LDS loads (ghost.hip): bf16, widths % 64 == 0.
 bool ghost_dma_ok(const dpsgd_layer& L);
+// Gram-form norms for float32 layers with 2 <= T <= 64 and widths % 64 == 0
+// (gram32.hip): one 64 x 64 tile per example, one partial per example.
+bool gram64_ok(const dpsgd_layer& L);
+int launch_gram64(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                  float* partials, int64_t P, hipStream_t stream);
 int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream);
 

@@ -305,9 +305,10 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
   int idx_gv[256], n_gv = 0;
   int idx_gs[256], n_gs = 0;
   int idx_gd[256], n_gd = 0;
+  int idx_g64[256], n_g64 = 0;
   int idx_mat[256], n_mat = 0;
   for (int base = 0; base < n_layers; base += 256) {
-    n_t1 = n_gv = n_gs = n_gd = n_mat = 0;
+    n_t1 = n_gv = n_gs = n_gd = n_g64 = n_mat = 0;
     const int m = n_layers - base < 256 ? n_layers - base : 256;
     for (int k = 0; k < m; ++k) {
       const int l = base + k;
@@ -316,6 +317,7 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
         case FORM_STORED: break;   // skinny.hip
         case FORM_GHOST:
           if (ghost_dma_ok(layers[l])) idx_gd[n_gd++] = l;
+          else if (gram64_ok(layers[l])) idx_g64[n_g64++] = l;
           else if (ghost_vec_ok<TIn>(layers[l])) idx_gv[n_gv++] = l;
           else idx_gs[n_gs++] = l;
           break;
@@ -329,6 +331,7 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
     if (st == DPSGD_OK && n_gs)
       st = launch_ghost_group<TIn, false>(layers, idx_gs, n_gs, cols, partials, P, stream);
     if (st == DPSGD_OK && n_gd) st = launch_ghost_dma(layers, idx_gd, n_gd, cols, partials, P, stream);
+    if (st == DPSGD_OK && n_g64) st = launch_gram64(layers, idx_g64, n_g64, cols, partials, P, stream);
     if (st == DPSGD_OK && n_mat)
       st = launch_mat_norms(layers, idx_mat, n_mat, cols, partials, P, stream);
     if (st != DPSGD_OK) return st;
@@ -345,8 +348,11 @@ NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode) {
   // AUTO: compare the MFMA work each form issues at tile granularity.
   const int64_t bk = L.dtype == DPSGD_BF16 ? TileCfg<uint16_t>::BK : TileCfg<float>::BK;
   const int64_t nt = ceil_div(L.T, kTile);
-  const double ghost = (double)(nt * (nt + 1) / 2) *
-                       (double)(ceil_div(L.d_in, bk) * bk + ceil_div(L.d_out, bk) * bk);
+  // (The float32 kernel for T <= 64 takes one 64 x 64 tile: a quarter of the
+  // 128 x 128 one.)
+  const double ghost = gram64_ok(L) ? (double)(L.d_in + L.d_out) / 4.0
+                                    : (double)(nt * (nt + 1) / 2) *
+                                          (double)(ceil_div(L.d_in, bk) * bk + ceil_div(L.d_out, bk) * bk);
   // (A k-major float32 tile, 64 x 256 or 128 x 128, has the area of a 128 x 128 one.)
   const int64_t mt = k32_ok(L) ? mat_tile_count(L) : ceil_div(L.d_out, kTile) * ceil_div(L.d_in, kTile);
   const double mat = (double)mt * (double)(ceil_div(L.T, bk) * bk);

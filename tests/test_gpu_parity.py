@@ -124,6 +124,8 @@ NORM_SHAPES = [
     (3, 64, 520, 60),      # float32 k-major kernel, 64 x 256 tiles, ragged in both widths
     (2, 96, 132, 260),     # float32 k-major kernel, 128 x 128 tiles, ragged in both widths
     (5, 64, 27, 16),       # stem-convolution widths: g_i formed on the VALU
+    (3, 64, 192, 128),     # float32 Gram form on one 64 x 64 tile (T = 64)
+    (2, 37, 128, 64),      # the same with rows past T (zeroed in LDS)
 ]
 
 
