@@ -510,19 +510,25 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
       }
     }
     if (skip) continue;
-    const float* S = lds + (int)((q - q0) & 1) * kK32StageFloats;
-    const float* pa0 = S + offa[0];
-    const float* pa1 = S + offa[1];
-    const float* pb0 = S + offb[0];
-    const float* pb1 = S + offb[1];
+    // A wave whose 64 x 64 block lies wholly past the output's edge (the
+    // last tile of a width that is not a multiple of the tile) has nothing
+    // to multiply: its accumulators stay 0 and its SIMD serves the other
+    // workgroup. It still takes part in the copies, barriers and partials.
+    if (m_base < E.M && n_base < E.N) {
+      const float* S = lds + (int)((q - q0) & 1) * kK32StageFloats;
+      const float* pa0 = S + offa[0];
+      const float* pa1 = S + offa[1];
+      const float* pb0 = S + offb[0];
+      const float* pb1 = S + offb[1];
 #pragma unroll
-    for (int kp = 0; kp < kK32Rows / 2; ++kp) {
-      const float a0 = pa0[2 * kp * TM], a1 = pa1[2 * kp * TM];
-      const float b0 = pb0[2 * kp * TN], b1 = pb1[2 * kp * TN];
-      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+      for (int kp = 0; kp < kK32Rows / 2; ++kp) {
+        const float a0 = pa0[2 * kp * TM], a1 = pa1[2 * kp * TM];
+        const float b0 = pb0[2 * kp * TN], b1 = pb1[2 * kp * TN];
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+      }
     }
     stored = false;
     if (EPI == EPI_SUMSQ && (q + 1) % spe == 0) {
