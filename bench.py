@@ -314,15 +314,16 @@ def main():
 
     # The same step captured once as a HIP graph and replayed (no per-call
     # launch overhead); reported beside the eager figure, not as `value`.
-    graph = dpsgd.StepGraph(Ls, buf, W.C, W.sigma, W.noise_seed, W.step, scale,
-                            dpsgd.DPSGD_NORM_AUTO, fused=args.fused)
-    for _ in range(args.warmup):
-        graph.replay()
+    # Every replay releases a fresh noise step.
+    graph = dpsgd.StepGraph(Ls, buf, W.C, W.sigma, scale, dpsgd.DPSGD_NORM_AUTO,
+                            fused=args.fused)
+    for k in range(args.warmup):
+        graph.replay(W.noise_seed, W.step + 1 + k)
     g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     g0.record()
-    for _ in range(args.steps):
-        graph.replay()
+    for k in range(args.steps):
+        graph.replay(W.noise_seed, W.step + 1 + args.warmup + k)
     g1.record()
     torch.cuda.synchronize()
     graph_ms = g0.elapsed_time(g1) / args.steps

@@ -58,7 +58,10 @@ typedef enum dpsgd_dtype {
 typedef enum dpsgd_norm_mode {
   DPSGD_NORM_AUTO = 0,         /* pick per layer by arithmetic cost           */
   DPSGD_NORM_GHOST = 1,        /* Gram form: sum_{t,s} (a_t.a_s)(g_t.g_s)     */
-  DPSGD_NORM_MATERIALIZE = 2   /* ||G_i^T A_i||_F^2, tile kept in registers   */
+  DPSGD_NORM_MATERIALIZE = 2,  /* ||G_i^T A_i||_F^2, tile kept in registers   */
+  DPSGD_NORM_CLOSED_FORM = 3   /* T = 1: ||a_i||^2 ||g_i||^2. Only reported by
+                                  dpsgd_select_norm_mode; not accepted as a
+                                  mode argument (DPSGD_ERR_UNSUPPORTED)       */
 } dpsgd_norm_mode;
 
 typedef enum dpsgd_status {
@@ -81,7 +84,8 @@ typedef struct dpsgd_layer {
   int64_t d_in;        /* >= 1                                                   */
   int64_t d_out;       /* >= 1                                                   */
   int32_t dtype;       /* dpsgd_dtype, shared by A and G                         */
-  uint32_t tensor_id;  /* third Philox counter word of this layer's noise        */
+  uint32_t tensor_id;  /* third Philox counter word of this layer's noise; the
+                          layers of one noise call must have distinct ids     */
 } dpsgd_layer;
 
 /* ---------------------------------------------------------------------------
@@ -96,14 +100,17 @@ typedef struct dpsgd_layer {
  *   mode      dpsgd_norm_mode, applied to every layer (AUTO picks per layer).
  *   norms_sq  float32 [B], device.
  *   workspace device scratch of at least dpsgd_norms_workspace_bytes(...)
- *             bytes (may be NULL when that value is 0); its contents on entry
- *             do not matter and are clobbered.
+ *             bytes, 16-byte aligned (DPSGD_ERR_INVALID_ARG otherwise); its
+ *             contents on entry do not matter and are clobbered.
  * T = 1 layers always use the closed form ||a||^2 ||g||^2 whatever the mode.
  * ------------------------------------------------------------------------- */
 size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode);
 
-/* The form AUTO selects for this layer (DPSGD_NORM_GHOST or _MATERIALIZE),
- * or a negative dpsgd_status for an invalid descriptor. */
+/* The form that dpsgd_per_example_norms[_multi] runs for this layer under
+ * DPSGD_NORM_AUTO: DPSGD_NORM_CLOSED_FORM for T = 1 (under every mode),
+ * otherwise DPSGD_NORM_GHOST or DPSGD_NORM_MATERIALIZE; or a negative
+ * dpsgd_status for an invalid descriptor. (In dpsgd_clipped_sum_multi a
+ * layer with a narrow side may take the stored form instead; see there.) */
 int32_t dpsgd_select_norm_mode(const dpsgd_layer* layer);
 
 int dpsgd_per_example_norms(const dpsgd_layer* layer, int32_t mode, float* norms_sq,
@@ -134,7 +141,8 @@ int dpsgd_clip_factors(const float* norms_sq, int64_t B, float C, float* factors
  * with c_i from dpsgd_clip_factors(norms_sq, B, C). factors_out / mask_out
  * (device, optional) receive c and the clip mask. The _multi form does the
  * same for n_layers layers (one grad buffer each, all with the same B) in one
- * grouped launch. workspace: at least dpsgd_clip_workspace_bytes(...) bytes.
+ * grouped launch. workspace: at least dpsgd_clip_workspace_bytes(...) bytes,
+ * 16-byte aligned (DPSGD_ERR_INVALID_ARG otherwise).
  * grad must be 16-byte aligned and must not alias any input.
  * ------------------------------------------------------------------------- */
 size_t dpsgd_clip_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers);
@@ -196,7 +204,11 @@ int dpsgd_clipped_sum_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t
  * v = (r>>8) 2^-24 for r1, r3; z_{4j+0,1} = sqrt(-2 ln u_a)(cos, sin)(2 pi v_a),
  * z_{4j+2,3} likewise from (u_b, v_b). sigma == 0 gives exactly scale*grad.
  * Reads only d_in, d_out and tensor_id of the layer descriptor.
- * sigma >= 0, C > 0 and finite, scale finite.
+ * sigma >= 0, C > 0 and finite, scale finite. The layers of one _multi call
+ * must have distinct tensor_ids (DPSGD_ERR_INVALID_ARG otherwise): layers
+ * with the same id would get the same normals. Independence across calls is
+ * the caller's: every (seed, tensor_id, step) must be used for one release
+ * only.
  * ------------------------------------------------------------------------- */
 int dpsgd_add_noise(const dpsgd_layer* layer, float* grad, float sigma, float C,
                     uint64_t seed, uint32_t step, float scale, void* stream);
@@ -224,7 +236,8 @@ int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* co
  * layer in each array; noisy_outs may be NULL (no layer writes g) or hold
  * NULL entries. The layer descriptor is read as in dpsgd_add_noise.
  * Errors (DPSGD_ERR_INVALID_ARG): a NULL or misaligned required pointer, the
- * noise arguments as in dpsgd_add_noise, lr < 0 or not finite, beta1 or beta2
+ * noise arguments as in dpsgd_add_noise (distinct tensor_ids included), lr < 0
+ * or not finite, beta1 or beta2
  * outside [0, 1), eps <= 0 or not finite, weight_decay < 0 or not finite,
  * t == 0.
  * ------------------------------------------------------------------------- */

@@ -138,7 +138,9 @@ def verify_step(params: VerifierParams, state: VerifierState, g_gpu: list[np.nda
     if state.aborted:
         raise RuntimeError("the run was already aborted")
     norm = math.sqrt(sum(float(np.sum(np.asarray(g, np.float64) ** 2)) for g in g_gpu))
-    if norm > params.C * (1.0 + params.norm_slack):
+    # Every threshold test below is written as "accepted only if within the
+    # bound", so a NaN (which is within no bound) is rejected.
+    if not norm <= params.C * (1.0 + params.norm_slack):
         state.aborted = True
         return StepOutcome(ABORT, STRUCTURAL, norm)
     if not coin:
@@ -152,14 +154,14 @@ def verify_step(params: VerifierParams, state: VerifierState, g_gpu: list[np.nda
             return StepOutcome(ABORT, BODY, norm, z32)
         return StepOutcome(ACCEPT, BODY, norm, z32)
     if params.rho_ill is not None:
-        if z32 > params.rho_ill:
+        if not z32 <= params.rho_ill:
             state.aborted = True
             return StepOutcome(ABORT, HARD, norm, z32)
         n_t = None
     else:
         r64 = ref64() if callable(ref64) else ref64
         n_t = params.B / (2.0 * params.C) * _dist(g_gpu, r64)
-        if n_t > params.tau_num:
+        if not n_t <= params.tau_num:
             state.aborted = True
             return StepOutcome(ABORT, HARD, norm, z32, n_t)
     state.S_amb += 1

@@ -2,6 +2,7 @@
 // The operations and their conventions are specified in include/dpsgd.h.
 #include <math.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "common.h"
@@ -82,6 +83,16 @@ size_t clip_ws_bytes(const dpsgd_layer* layers, int32_t n) {
 
 bool bad_float(float x) { return isnan(x); }
 
+// The noise of a layer is a function of (seed, tensor_id, step, element):
+// two layers of one call with the same tensor_id would receive the same
+// normals, and their difference would cancel the noise.
+bool distinct_tensor_ids(const dpsgd_layer* layers, int32_t n) {
+  std::vector<uint32_t> ids((size_t)n);
+  for (int32_t l = 0; l < n; ++l) ids[(size_t)l] = layers[l].tensor_id;
+  std::sort(ids.begin(), ids.end());
+  return std::adjacent_find(ids.begin(), ids.end()) == ids.end();
+}
+
 // Plan of dpsgd_clipped_sum_multi. Workspace: norm partials [B][P], then the
 // clip workspace of the other layers (factors first), then the stored
 // per-example gradients of the FORM_STORED layers.
@@ -153,8 +164,11 @@ size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, 
 int32_t dpsgd_select_norm_mode(const dpsgd_layer* layer) {
   const int st = check_layer(layer, false);
   if (st != DPSGD_OK) return st;
-  return resolve_norm_form(*layer, DPSGD_NORM_AUTO) == FORM_MAT ? DPSGD_NORM_MATERIALIZE
-                                                               : DPSGD_NORM_GHOST;
+  switch (resolve_norm_form(*layer, DPSGD_NORM_AUTO)) {
+    case FORM_T1: return DPSGD_NORM_CLOSED_FORM;
+    case FORM_MAT: return DPSGD_NORM_MATERIALIZE;
+    default: return DPSGD_NORM_GHOST;
+  }
 }
 
 int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode,
@@ -166,6 +180,7 @@ int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, i
   if (!norms_sq) return DPSGD_ERR_INVALID_ARG;
   const NormPlan p = plan_norms(layers, n_layers, mode);
   if (!workspace || workspace_bytes < p.bytes) return DPSGD_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return DPSGD_ERR_INVALID_ARG;
   return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
                       static_cast<float*>(workspace), p.P, p.cols.data(),
                       static_cast<hipStream_t>(stream));
@@ -203,6 +218,7 @@ int dpsgd_clip_accumulate_multi(const dpsgd_layer* layers, int32_t n_layers,
   if (bad_float(C) || !(C > 0.0f)) return DPSGD_ERR_INVALID_ARG;
   const size_t need = clip_ws_bytes(layers, n_layers);
   if (!workspace || workspace_bytes < need) return DPSGD_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return DPSGD_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t B = layers[0].B;
   float* factors = static_cast<float*>(workspace);
@@ -309,6 +325,7 @@ int dpsgd_add_noise_multi(const dpsgd_layer* layers, int32_t n_layers, float* co
   if (bad_float(sigma) || sigma < 0.0f || isinf(sigma)) return DPSGD_ERR_INVALID_ARG;
   if (bad_float(C) || !(C > 0.0f) || isinf(C)) return DPSGD_ERR_INVALID_ARG;
   if (!isfinite(scale)) return DPSGD_ERR_INVALID_ARG;
+  if (!distinct_tensor_ids(layers, n_layers)) return DPSGD_ERR_INVALID_ARG;
   return launch_noise(layers, n_layers, grads, sigma, C, seed, step, scale,
                       static_cast<hipStream_t>(stream));
 }
@@ -343,6 +360,7 @@ int dpsgd_noise_adamw_multi(const dpsgd_layer* layers, int32_t n_layers,
   if (!isfinite(o.eps) || !(o.eps > 0.0f)) return DPSGD_ERR_INVALID_ARG;
   if (!isfinite(o.weight_decay) || o.weight_decay < 0.0f) return DPSGD_ERR_INVALID_ARG;
   if (o.t == 0) return DPSGD_ERR_INVALID_ARG;
+  if (!distinct_tensor_ids(layers, n_layers)) return DPSGD_ERR_INVALID_ARG;
   return launch_noise_adamw(layers, n_layers, grads, params, exp_avgs, exp_avg_sqs, noisy_outs,
                             sigma, C, seed, step, scale, o, static_cast<hipStream_t>(stream));
 }

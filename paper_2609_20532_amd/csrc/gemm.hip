@@ -475,7 +475,6 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   // Output v of block (a, b) in this lane: row 8 (v / 4) + 4 h + v % 4 and
   // column l % 32 of the block.
   const int m_base = tmi * TM + wm * 64, n_base = tni * TN + wn * 64;
-  bool stored = false;   // EPI_SUMSQ: a partial was stored after the last copies
 
   if (EPI == EPI_SUMSQ && ((tmi + 1) * TM > E.M || (tni + 1) * TN > E.N)) {
     // Edge tile: clear both slice buffers once (see issue()).
@@ -485,12 +484,12 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
   }
   if (q0 < q1) issue(q0, 0);
   for (int64_t q = q0; q < q1; ++q) {
-    // Slice q is complete for this wave once nothing is outstanding but the
-    // partial stored after its copies were issued (loads and stores complete
-    // in order); the barrier makes every wave's copies visible and guarantees
-    // that slice q - 1, whose buffer is refilled next, is no longer read.
-    if (EPI == EPI_SUMSQ && stored) wait_vmcnt<1>();
-    else wait_vmcnt<0>();
+    // Slice q is complete for this wave once none of its vector-memory
+    // operations is outstanding (its copies, and a partial stored at the end
+    // of the previous example); the barrier makes every wave's copies visible
+    // and guarantees that slice q - 1, whose buffer is refilled next, is no
+    // longer read.
+    wait_vmcnt<0>();
     barrier_no_wait();
     if (q + 1 < q1) issue(q + 1, (int)((q + 1 - q0) & 1));
     bool skip = false;
@@ -530,7 +529,6 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
         acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
       }
     }
-    stored = false;
     if (EPI == EPI_SUMSQ && (q + 1) % spe == 0) {
       // End of an example: this wave's share of ||G_i^T A_i||_F^2 over the
       // tile (entries past the edges are exactly 0), one partial per wave.
@@ -547,7 +545,6 @@ __global__ __launch_bounds__(kThreads, 2) void tgemm_k32_kernel(K32Args args) {
       s = wave_sum(s);
       if (lane == 0)
         args.partials[(q / spe) * args.P + E.partial_col + 4 * tile + wave] = s;
-      stored = true;
     }
   }
 

@@ -2,8 +2,9 @@
 //
 // Paper: Section "Two-Stage Verification", algorithm "TEE Verification", and
 // the clipped average of Section 2.2. The recomputation is the verifier's own
-// float32 / float64 implementation of the clipped average; the decision rule
-// follows the algorithm step by step (see dpsgd_verifier.h).
+// float32 / float64 implementation of the clipped average. A step is first
+// classified from the thresholds (structural, unchecked, body, hard or
+// ambiguity), then charged to the one ledger of its class.
 //
 // Determinism: every reduction has a fixed order that does not depend on the
 // thread count. Squared norms are per example (one task per example, layers
@@ -261,15 +262,25 @@ bool params_ok(const dpsgd_verifier_params* p) {
          (p->rho_amb > 0.0 || p->rho_ill > 0.0);
 }
 
-double distance(const dpsgd_layer* layers, int n, const float* const* g, const void* const* r,
-                bool r_is_double) {
+// ||g - ref||_2 over all layers, where ref is the verifier's own clipped
+// average recomputed in T (float or double). *status receives the
+// recomputation's status.
+template <typename T>
+double distance_to_reference(const dpsgd_layer* layers, int n, const float* const* g, double C,
+                             int64_t B, int threads, int* status) {
+  std::vector<std::vector<T>> ref((size_t)n);
+  std::vector<T*> ptr((size_t)n);
+  for (int l = 0; l < n; ++l) {
+    ref[(size_t)l].resize((size_t)(layers[l].d_out * layers[l].d_in));
+    ptr[(size_t)l] = ref[(size_t)l].data();
+  }
+  *status = reference_mean<T>(layers, n, (T)C, B, ptr.data(), threads);
+  if (*status != DPSGD_OK) return 0.0;
   double s = 0.0;
   for (int l = 0; l < n; ++l) {
     const int64_t e = layers[l].d_out * layers[l].d_in;
     for (int64_t j = 0; j < e; ++j) {
-      const double rv = r_is_double ? static_cast<const double*>(r[l])[j]
-                                    : (double)static_cast<const float*>(r[l])[j];
-      const double d = (double)g[l][j] - rv;
+      const double d = (double)g[l][j] - (double)ref[(size_t)l][(size_t)j];
       s += d * d;
     }
   }
@@ -307,66 +318,57 @@ int dpsgd_verify_step(const dpsgd_verifier_params* params, dpsgd_verifier_state*
   const double nan = std::numeric_limits<double>::quiet_NaN();
   dpsgd_verify_result r{DPSGD_VERIFY_ACCEPT, DPSGD_PATH_UNCHECKED, 0.0, nan, nan};
   const double C = params->C;
+  // Each bound below accepts only a value within it, so NaN never passes.
+  auto within = [](double v, double bound) { return v <= bound; };
 
-  // Structural invariant (every step, before the coin).
+  // 1. Classify the step. The norm bound holds for every honest clipped
+  //    average, so it is tested on every submission, before the coin.
   double nsq = 0.0;
   for (int l = 0; l < n_layers; ++l) {
     const int64_t e = layers[l].d_out * layers[l].d_in;
     for (int64_t j = 0; j < e; ++j) nsq += (double)g_gpu[l][j] * (double)g_gpu[l][j];
   }
   r.norm = std::sqrt(nsq);
-  ++state->steps;
-  auto finish = [&](int decision, int path) {
-    r.decision = decision;
-    r.path = path;
-    if (decision == DPSGD_VERIFY_ABORT) state->aborted = 1;
-    *result = r;
-    return (int)DPSGD_OK;
-  };
-  if (!(r.norm <= C * (1.0 + params->norm_slack)))
-    return finish(DPSGD_VERIFY_ABORT, DPSGD_PATH_STRUCTURAL);
-  if (!coin) return finish(DPSGD_VERIFY_ACCEPT, DPSGD_PATH_UNCHECKED);
-  ++state->checked;
-
-  // Body path against the float32 recomputation.
-  std::vector<std::vector<float>> r32((size_t)n_layers);
-  std::vector<float*> p32((size_t)n_layers);
-  for (int l = 0; l < n_layers; ++l) {
-    r32[(size_t)l].resize((size_t)(layers[l].d_out * layers[l].d_in));
-    p32[(size_t)l] = r32[(size_t)l].data();
-  }
-  int st = dpsgd_reference_mean_f32(layers, n_layers, (float)C, params->B, p32.data(), threads);
-  if (st != DPSGD_OK) return st;
-  r.z32 = distance(layers, n_layers, g_gpu, reinterpret_cast<const void* const*>(p32.data()),
-                   false) / C;
-  if (r.z32 <= params->tau_abs) {
-    state->Z_sub += r.z32;
-    return finish(state->Z_sub > params->K_sub ? DPSGD_VERIFY_ABORT : DPSGD_VERIFY_ACCEPT,
-                  DPSGD_PATH_BODY);
-  }
-
-  // Escalation: the float64 layer, or the hard cap of a family without it.
-  if (params->rho_amb > 0.0) {
-    r32.clear();
-    std::vector<std::vector<double>> r64((size_t)n_layers);
-    std::vector<double*> p64((size_t)n_layers);
-    for (int l = 0; l < n_layers; ++l) {
-      r64[(size_t)l].resize((size_t)(layers[l].d_out * layers[l].d_in));
-      p64[(size_t)l] = r64[(size_t)l].data();
-    }
-    st = dpsgd_reference_mean_f64(layers, n_layers, C, params->B, p64.data(), threads);
+  int path;
+  if (!within(r.norm, C * (1.0 + params->norm_slack))) {
+    path = DPSGD_PATH_STRUCTURAL;
+  } else if (!coin) {
+    path = DPSGD_PATH_UNCHECKED;
+  } else {
+    int st = DPSGD_OK;
+    r.z32 = distance_to_reference<float>(layers, n_layers, g_gpu, C, params->B, threads, &st) / C;
     if (st != DPSGD_OK) return st;
-    const double d64 = distance(layers, n_layers, g_gpu,
-                                reinterpret_cast<const void* const*>(p64.data()), true);
-    r.n_t = (double)params->B / (2.0 * C) * d64;
-    if (!(r.n_t <= params->rho_amb * (double)params->B / 2.0))
-      return finish(DPSGD_VERIFY_ABORT, DPSGD_PATH_HARD);
-  } else if (!(r.z32 <= params->rho_ill)) {
-    return finish(DPSGD_VERIFY_ABORT, DPSGD_PATH_HARD);
+    if (within(r.z32, params->tau_abs)) {
+      path = DPSGD_PATH_BODY;
+    } else if (params->rho_amb > 0.0) {
+      // Escalation to the float64 recomputation, in the accountant's units.
+      r.n_t = (double)params->B / (2.0 * C) *
+              distance_to_reference<double>(layers, n_layers, g_gpu, C, params->B, threads, &st);
+      if (st != DPSGD_OK) return st;
+      path = within(r.n_t, params->rho_amb * (double)params->B / 2.0) ? DPSGD_PATH_AMBIGUITY
+                                                                      : DPSGD_PATH_HARD;
+    } else {
+      // A family without the float64 layer: a hard cap on z32 instead.
+      path = within(r.z32, params->rho_ill) ? DPSGD_PATH_AMBIGUITY : DPSGD_PATH_HARD;
+    }
   }
-  ++state->S_amb;
-  return finish(state->S_amb > params->K_amb ? DPSGD_VERIFY_ABORT : DPSGD_VERIFY_ACCEPT,
-                DPSGD_PATH_AMBIGUITY);
+
+  // 2. One ledger update for the class, and the decision.
+  ++state->steps;
+  bool abort = path == DPSGD_PATH_STRUCTURAL || path == DPSGD_PATH_HARD;
+  if (path != DPSGD_PATH_STRUCTURAL && path != DPSGD_PATH_UNCHECKED) ++state->checked;
+  if (path == DPSGD_PATH_BODY) {
+    state->Z_sub += r.z32;
+    abort = state->Z_sub > params->K_sub;
+  } else if (path == DPSGD_PATH_AMBIGUITY) {
+    ++state->S_amb;
+    abort = state->S_amb > params->K_amb;
+  }
+  r.path = path;
+  r.decision = abort ? DPSGD_VERIFY_ABORT : DPSGD_VERIFY_ACCEPT;
+  if (abort) state->aborted = 1;
+  *result = r;
+  return DPSGD_OK;
 }
 
 }  // extern "C"

@@ -22,6 +22,7 @@ DPSGD_BF16 = 1
 DPSGD_NORM_AUTO = 0
 DPSGD_NORM_GHOST = 1
 DPSGD_NORM_MATERIALIZE = 2
+DPSGD_NORM_CLOSED_FORM = 3   # reported by dpsgd_select_norm_mode for T = 1 layers
 
 DPSGD_OK = 0
 DPSGD_ERR_INVALID_ARG = -1
@@ -146,8 +147,11 @@ def _ptr(t):
 # ----------------------------------------------------------------- descriptors
 
 
-def make_layer(A, G, tensor_id: int = 0) -> dpsgd_layer:
-    """Descriptor of one layer from device tensors A [B,T,d_in] and G [B,T,d_out]."""
+def make_layer(A, G, tensor_id: int) -> dpsgd_layer:
+    """Descriptor of one layer from device tensors A [B,T,d_in] and G [B,T,d_out].
+
+    ``tensor_id`` selects the layer's noise stream: the layers of one step
+    need distinct ids (the noise calls reject repeats)."""
     import torch
     if A.dim() != 3 or G.dim() != 3 or A.shape[:2] != G.shape[:2]:
         raise ValueError("A must be [B,T,d_in] and G [B,T,d_out] with the same B, T")
@@ -359,10 +363,10 @@ def alloc_step(layers, mode: int = DPSGD_NORM_AUTO, device="cuda", fused: bool =
     )
 
 
-def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
-             scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, stream=None, fused: bool = False):
-    """One DP-SGD gradient step: global norms, clip + sum, noise (three ABI
-    calls, or two with ``fused``: dpsgd_clipped_sum_multi, then the noise)."""
+def run_clipped_sum(layers, buf: StepBuffers, C: float, mode: int = DPSGD_NORM_AUTO, stream=None,
+                    fused: bool = False):
+    """The step up to its commit point: global norms, clip factors and the
+    clipped sums in ``buf.grads`` (two ABI calls, or one with ``fused``)."""
     if fused:
         dpsgd_clipped_sum_multi(layers, mode, C, buf.grads, buf.norms_sq, accumulate=False,
                                 factors_out=buf.factors, mask_out=buf.mask,
@@ -373,35 +377,54 @@ def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: 
         dpsgd_clip_accumulate_multi(layers, buf.norms_sq, C, buf.grads, accumulate=False,
                                     factors_out=buf.factors, mask_out=buf.mask,
                                     workspace=buf.clip_ws, stream=stream)
+
+
+def run_step(layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
+             scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, stream=None, fused: bool = False):
+    """One DP-SGD gradient step: global norms, clip + sum, noise (three ABI
+    calls, or two with ``fused``: dpsgd_clipped_sum_multi, then the noise)."""
+    run_clipped_sum(layers, buf, C, mode, stream, fused)
     dpsgd_add_noise_multi(layers, buf.grads, sigma, C, seed, step, scale, stream=stream)
 
 
 class StepGraph:
-    """One step captured as a HIP graph (torch.cuda.CUDAGraph) and replayed.
+    """The clipped-sum part of a step captured as a HIP graph (torch.cuda.CUDAGraph),
+    replayed once per step, followed by the noise call.
 
     The library makes no allocation, memset or synchronising call while it
-    enqueues a step, so the whole step can be captured. A replay re-runs every
-    kernel with the arguments of the capture: the same input and output
-    buffers (refill the inputs in place between replays), and the same C,
-    sigma, seed, step and scale (a replay for another noise step needs a new
-    capture). It removes the per-call launch overhead, which dominates steps of
-    small layers."""
+    enqueues, so the norms, factors and clipped sums (two ABI calls, or one
+    with ``fused``) can be captured. A replay re-runs them with the arguments
+    of the capture: the same input and output buffers (refill the inputs in
+    place between replays) and the same C. The noise is not captured: it is
+    enqueued after each replay with the seed and step that ``replay`` is
+    given, because a captured noise kernel would add the same normals at
+    every replay. A (seed, step) pair that this object has already released
+    is refused: the noise of every release must be fresh."""
 
-    def __init__(self, layers, buf: StepBuffers, C: float, sigma: float, seed: int, step: int = 0,
-                 scale: float = 1.0, mode: int = DPSGD_NORM_AUTO, fused: bool = False):
+    def __init__(self, layers, buf: StepBuffers, C: float, sigma: float, scale: float = 1.0,
+                 mode: int = DPSGD_NORM_AUTO, fused: bool = False):
         import torch
         load()
         self._keep = (layers, buf)
+        self._noise = (sigma, C, scale)
+        self._used = set()
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):   # one eager step first, outside the capture
-            run_step(layers, buf, C, sigma, seed, step, scale, mode, fused=fused)
+        with torch.cuda.stream(side):   # one eager pass first, outside the capture
+            run_clipped_sum(layers, buf, C, mode, fused=fused)
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
-            run_step(layers, buf, C, sigma, seed, step, scale, mode, fused=fused)
+            run_clipped_sum(layers, buf, C, mode, fused=fused)
 
-    def replay(self):
+    def replay(self, seed: int, step: int):
+        """One step: the captured clipped sums, then noise keyed by (seed, step)."""
+        key = (int(seed), int(step))
+        if key in self._used:
+            raise ValueError(f"noise (seed, step) = {key} was already released by this graph")
+        self._used.add(key)
+        layers, buf = self._keep
+        sigma, C, scale = self._noise
         self.graph.replay()
-
+        dpsgd_add_noise_multi(layers, buf.grads, sigma, C, seed, step, scale)

@@ -78,3 +78,96 @@ def assert_sum_close(got, ref, tol: float, what: str = ""):
 def guard_band(norms_ref: np.ndarray, C: float, tol: float) -> np.ndarray:
     """Examples whose oracle norm is within tol of C (clip decision not pinned)."""
     return np.abs(norms_ref / C - 1.0) <= tol
+
+
+# ------------------------------------------------------------- whole-step checks
+
+# Bounds on the Frobenius-relative error of a clipped sum before noise, from
+# the arithmetic: float32 accumulation with every clip weight applied in
+# float32, or one bfloat16 rounding of c_i * G on the MFMA operand.
+SUM_BOUND_FP32_WEIGHTS = 2e-5
+SUM_BOUND_BF16_WEIGHTS = 5e-3
+
+
+def stored_form(T: int, d_in: int, d_out: int, dtype: str) -> bool:
+    """Whether the one-call step (dpsgd_clipped_sum_multi, AUTO) stores this
+    layer's per-example gradients: narrow side <= 16, wide side a multiple of
+    4 (at most 2^30) and 4 d_in d_out float32 bytes at most a quarter of the
+    per-example input bytes."""
+    narrow, wide = min(d_in, d_out), max(d_in, d_out)
+    elem = 2 if dtype == wl.BF16 else 4
+    return (narrow <= 16 and wide % 4 == 0 and wide <= (1 << 30)
+            and 4 * 4 * d_in * d_out <= T * (d_in + d_out) * elem)
+
+
+def weights_in_fp32(T: int, d_in: int, d_out: int, dtype: str, fused: bool = False) -> bool:
+    """True when the library applies every clip weight in float32 on this
+    layer (no bfloat16 rounding of c_i * G): float32 inputs; the stored form;
+    layers whose g_i has at most 512 entries (formed on the VALU); the 256-
+    and 384x256-tile kernels; the 128-tile kernel when T needs at most 1/8 of
+    zero padding to a multiple of its 64-row K step."""
+    if dtype == wl.F32:
+        return True
+    if fused and stored_form(T, d_in, d_out, dtype):
+        return True
+    if d_in * d_out <= 512:
+        return True
+    big = d_in % 256 == 0 and (d_out % 256 == 0 or d_out % 384 == 0) and T % 32 == 0
+    return big or (T >= 64 and (-T) % 64 * 8 <= T)
+
+
+def sum_bound(T: int, d_in: int, d_out: int, dtype: str, fused: bool = False) -> float:
+    return (SUM_BOUND_FP32_WEIGHTS if weights_in_fp32(T, d_in, d_out, dtype, fused)
+            else SUM_BOUND_BF16_WEIGHTS)
+
+
+def check_step_outputs(*, norms_sq, mask, sums, noised, res, C: float, tol: float, bounds,
+                       what: str = ""):
+    """Checks one step's GPU outputs against the oracle's StepResult `res`.
+
+    norms_sq, mask: the GPU's [B] arrays; sums: the clipped sums copied before
+    the noise call; noised: the outputs after it (float64 arrays, one per
+    layer); bounds: per layer, the error bound of its clipped sum before
+    noise (sum_bound). Asserts:
+      * every example's norm within min(tol, 1e-4) relative;
+      * the clip mask bit-exact outside the guard band around C;
+      * each clipped sum before noise within its bound (and within tol);
+      * each noised output within tol;
+      * Section 2.2's clip: every example contributes at most C, so the
+        global norm of the sums is at most B C (the structural check); with
+        one example whose norm exceeds C it equals C.
+    Returns the largest relative error of the sums before noise."""
+    B = len(res.norms)
+    n_gpu = np.sqrt(np.asarray(norms_sq, np.float64))
+    nerr = float(np.max(np.abs(n_gpu - res.norms) / res.norms))
+    assert nerr <= min(tol, 1e-4), f"{what}: norm error {nerr:.2e}"
+    band = guard_band(res.norms, C, tol)
+    np.testing.assert_array_equal(np.asarray(mask)[~band], res.mask[~band],
+                                  err_msg=f"{what}: clip mask")
+    worst = 0.0
+    for k, (s, ref) in enumerate(zip(sums, res.sums)):
+        r = assert_sum_close(s, ref, min(tol, bounds[k]), f"{what}: layer {k} clipped sum")
+        worst = max(worst, r)
+    for k, (g, ref) in enumerate(zip(noised, res.noised)):
+        assert_sum_close(g, ref, tol, f"{what}: layer {k} noised output")
+    total = float(np.sqrt(sum(float(np.sum(np.asarray(s, np.float64) ** 2)) for s in sums)))
+    # The factors come from the GPU's own norms (within 1e-4 of the oracle's).
+    slack = max(bounds) + 1e-4
+    assert total <= B * C * (1.0 + slack), f"{what}: ||S|| = {total:.6e} > B C"
+    if B == 1 and res.mask[0] == 1 and not band[0]:
+        assert abs(total / C - 1.0) <= slack, (
+            f"{what}: one clipped example, ||S|| / C = {total / C:.8f}, not 1")
+    return worst
+
+
+def run_step_keep_sums(dp, Ls, buf, C, sigma, seed, step, scale, mode=0, fused=False):
+    """Runs a step through the ABI and returns (sums before noise, noised
+    outputs) as float64 host arrays: the clipped sums are copied between the
+    clip call and the noise call."""
+    import torch
+    dp.run_clipped_sum(Ls, buf, C, mode, fused=fused)
+    torch.cuda.synchronize()
+    sums = [torch_to_float64(g) for g in buf.grads]
+    dp.dpsgd_add_noise_multi(Ls, buf.grads, sigma, C, seed, step, scale)
+    torch.cuda.synchronize()
+    return sums, [torch_to_float64(g) for g in buf.grads]

@@ -228,3 +228,54 @@ def test_fused_workspace_holds_the_stored_gradients(lib):
     assert dpsgd.dpsgd_clipped_sum_workspace_bytes(wide, dpsgd.DPSGD_NORM_GHOST) == \
         dpsgd.dpsgd_clipped_sum_workspace_bytes(wide)
     assert dpsgd.dpsgd_clipped_sum_workspace_bytes([dpsgd.shape_layer(0, 1, 4, 4)]) == 0
+
+
+def test_select_norm_mode_reports_the_closed_form_for_T1(lib):
+    """T = 1 layers run ||a||^2 ||g||^2 under every mode, and the query says so."""
+    for d_in, d_out in ((256, 128), (784, 512), (4096, 16)):
+        L = dpsgd.shape_layer(32, 1, d_in, d_out, dpsgd.DPSGD_F32)
+        assert dpsgd.dpsgd_select_norm_mode(L) == dpsgd.DPSGD_NORM_CLOSED_FORM
+    # The reported value is not a mode argument.
+    L = _lay()
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), dpsgd.DPSGD_NORM_CLOSED_FORM,
+                                       ctypes.c_void_p(64), 0, ctypes.c_void_p(128), 1 << 20,
+                                       None) == -2
+    assert dpsgd.dpsgd_norms_workspace_bytes(L, dpsgd.DPSGD_NORM_CLOSED_FORM) == 0
+
+
+def test_norms_and_clip_reject_misaligned_workspace(lib):
+    L = _lay()
+    assert lib.dpsgd_per_example_norms(ctypes.byref(L), 0, ctypes.c_void_p(64), 0,
+                                       ctypes.c_void_p(136), 1 << 20, None) == -1
+    arr = (dpsgd.dpsgd_layer * 2)(_lay(), _lay(tensor_id=1))
+    assert lib.dpsgd_per_example_norms_multi(arr, 2, 0, ctypes.c_void_p(64), 0,
+                                             ctypes.c_void_p(520), 1 << 20, None) == -1
+    assert lib.dpsgd_clip_accumulate(ctypes.byref(L), ctypes.c_void_p(64), 1.0,
+                                     ctypes.c_void_p(256), 0, None, None, ctypes.c_void_p(516),
+                                     1 << 20, None) == -1
+    g = (ctypes.c_void_p * 2)(ctypes.c_void_p(256), ctypes.c_void_p(512))
+    assert lib.dpsgd_clip_accumulate_multi(arr, 2, ctypes.c_void_p(64), 1.0, g, 0, None, None,
+                                           ctypes.c_void_p(1032), 1 << 20, None) == -1
+
+
+def test_noise_calls_reject_repeated_tensor_ids(lib):
+    """Two layers of one noise call with the same tensor_id would receive the
+    same normals; the call refuses them before enqueuing anything."""
+    dup = (dpsgd.dpsgd_layer * 3)(_lay(tensor_id=0), _lay(tensor_id=5), _lay(tensor_id=0))
+    ok = (dpsgd.dpsgd_layer * 3)(_lay(tensor_id=0), _lay(tensor_id=5), _lay(tensor_id=1))
+    g = (ctypes.c_void_p * 3)(*[ctypes.c_void_p(256 * (k + 1)) for k in range(3)])
+    assert lib.dpsgd_add_noise_multi(dup, 3, g, 1.0, 1.0, 1, 0, 1.0, None) == -1
+    opt = dpsgd.make_adamw(**_GOOD_ADAMW)
+    arrs = [(ctypes.c_void_p * 3)(*[ctypes.c_void_p(4096 * (j + 1) + 256 * k) for k in range(3)])
+            for j in range(4)]
+    assert lib.dpsgd_noise_adamw_multi(dup, 3, *arrs, None, 1.0, 1.0, 1, 0, 1.0,
+                                       ctypes.byref(opt), None) == -1
+    # The same arrays with distinct ids pass the checks (a NULL stream would
+    # then launch, so only the argument checks are exercised here: sigma < 0).
+    assert lib.dpsgd_add_noise_multi(ok, 3, g, -1.0, 1.0, 1, 0, 1.0, None) == -1
+
+
+def test_make_layer_requires_a_tensor_id():
+    import inspect
+    p = inspect.signature(dpsgd.make_layer).parameters["tensor_id"]
+    assert p.default is inspect.Parameter.empty

@@ -1,9 +1,11 @@
-"""A whole step captured as a HIP graph and replayed: every replay equals an
-eager step on the same inputs bit for bit (the kernels are deterministic),
-with eager work (refilling the inputs in place) and synchronisations between
-replays. Covers the T = 1 closed form, the 128-tile, 256-tile and 384x256-tile
-kernels, the Gram-form norms, the split-K fix-ups and the fused call's stored
-per-example gradients."""
+"""The clipped-sum part of a step captured as a HIP graph and replayed, with
+a fresh noise step enqueued after each replay: every replay plus its noise
+equals an eager step on the same inputs bit for bit (the kernels are
+deterministic), with eager work (refilling the inputs in place) and
+synchronisations between replays. Covers the T = 1 closed form, the 128-tile,
+256-tile and 384x256-tile kernels, the Gram-form norms, the split-K fix-ups
+and the fused call's stored per-example gradients. A (seed, step) pair
+already released is refused."""
 
 import sys
 
@@ -54,17 +56,18 @@ def test_graph_replays_equal_eager_steps(dp, name, B, dtype, dims, fused):
           for k, (T, di, do) in enumerate(dims)]
     dev = device_layers(hs)   # keeps the device tensors alive
     Ls = [d[0] for d in dev]
-    C, sigma, seed, step, scale = 0.5, 0.8, 1234, 3, 1.0 / B
+    C, sigma, seed, scale = 0.5, 0.8, 1234, 1.0 / B
     buf_g = dp.alloc_step(Ls, fused=fused)
     buf_e = dp.alloc_step(Ls, fused=fused)
-    graph = dp.StepGraph(Ls, buf_g, C, sigma, seed, step, scale, fused=fused)
+    graph = dp.StepGraph(Ls, buf_g, C, sigma, scale, fused=fused)
     for r in range(3):
         # Eager work between replays: new inputs in the same buffers.
         for _, A, G in dev:
             A.mul_(1.0 + 0.25 * (r + 1))
             G.add_(0.01 * (r + 1))
         torch.cuda.synchronize()
-        graph.replay()
+        step = 3 + r   # a fresh noise step per replay
+        graph.replay(seed, step)
         torch.cuda.synchronize()
         dp.run_step(Ls, buf_e, C, sigma, seed, step, scale, fused=fused)
         torch.cuda.synchronize()
@@ -74,3 +77,6 @@ def test_graph_replays_equal_eager_steps(dp, name, B, dtype, dims, fused):
             np.testing.assert_array_equal(a.cpu().numpy(), b.cpu().numpy(),
                                           err_msg=f"{name}: replay {r}, layer {k}")
         _log(f"{name}: replay {r} equals the eager step")
+    # A released (seed, step) is not released twice.
+    with pytest.raises(ValueError):
+        graph.replay(seed, 3)

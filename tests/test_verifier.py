@@ -182,10 +182,16 @@ def test_structural_invariant_before_the_coin(lib):
     assert _both(cp, op, cst, ost, hosts, ref32, ref64, inside, 0).path == V.DPSGD_PATH_UNCHECKED
     r = _both(cp, op, cst, ost, hosts, ref32, ref64, over, 0)
     assert r.path == V.DPSGD_PATH_STRUCTURAL and r.decision == V.DPSGD_VERIFY_ABORT
-    nan = [x.copy() for x in ref32]
-    nan[0][0, 0] = np.nan
-    cst = V.dpsgd_verifier_init(cp)
-    assert V.dpsgd_verify_step(cp, cst, hosts, nan, 0).path == V.DPSGD_PATH_STRUCTURAL
+    # A NaN submission fails the structural check in both verifiers, whatever the coin.
+    for coin in (0, 1):
+        nan = [x.copy() for x in ref32]
+        nan[0][0, 0] = np.nan
+        cst, ost = V.dpsgd_verifier_init(cp), vo.VerifierState()
+        out = vo.verify_step(op, ost, [x.astype(np.float64) for x in nan], coin, ref32, ref64)
+        res = V.dpsgd_verify_step(cp, cst, hosts, nan, coin)
+        assert out.path == vo.STRUCTURAL and out.decision == vo.ABORT and ost.aborted
+        assert res.path == V.DPSGD_PATH_STRUCTURAL and res.decision == V.DPSGD_VERIFY_ABORT
+        assert math.isnan(res.norm) and math.isnan(out.norm)
 
 
 def test_ledgers_run_out_like_the_oracle(lib):
