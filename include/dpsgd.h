@@ -21,7 +21,9 @@
  *    of W itself).
  *  - Every pointer to tensor data is a DEVICE pointer owned by the caller.
  *    The library allocates no device memory, keeps no pointer after a call
- *    returns and holds no mutable global state; calls are thread-safe.
+ *    returns and holds no mutable global state; calls are thread-safe. The
+ *    one exception is dpsgd_per_example_norms_multi_noalloc, whose scratch
+ *    array lives in each GPU's memory (see there).
  *  - Arrays of descriptors (dpsgd_layer*, float* const*) are HOST memory and
  *    are read before the call returns.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
@@ -120,6 +122,37 @@ int dpsgd_per_example_norms(const dpsgd_layer* layer, int32_t mode, float* norms
 int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t mode,
                                   float* norms_sq, int32_t accumulate, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Per-example norms with no workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.
+ *
+ * The operation, arguments and results of dpsgd_per_example_norms_multi
+ * (bit for bit: the same kernels run), with the per-example partials kept
+ * in a scratch array of DPSGD_NOALLOC_SCRATCH_BYTES bytes that the library
+ * holds in the memory of each GPU it runs on, from the first call on that
+ * GPU until the process ends. The call allocates nothing.
+ *  - Runs on the current device (hipSetDevice), whose stream `stream` must be.
+ *    The first call on a device resolves the array's address there (no
+ *    stream work); make it before capturing a graph that contains the call.
+ *  - DPSGD_ERR_WORKSPACE when the layers need more partial storage than the
+ *    array holds (dpsgd_norms_workspace_bytes(layers, n, mode) >
+ *    DPSGD_NOALLOC_SCRATCH_BYTES, i.e. about 2M partials: B times the sum
+ *    over layers of the partials per example); checked before anything else
+ *    touches the device. DPSGD_ERR_HIP when the runtime cannot give the
+ *    array's address on the current device. Other errors as in
+ *    dpsgd_per_example_norms_multi.
+ *  - Every call on one GPU uses that GPU's one array, which keeps the last
+ *    call's partials: calls that overlap in time on one GPU (different
+ *    streams, or host threads without ordering between them) race, and
+ *    their results are undefined.
+ * ------------------------------------------------------------------------- */
+#define DPSGD_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+
+int dpsgd_per_example_norms_multi_noalloc(const dpsgd_layer* layers, int32_t n_layers,
+                                          int32_t mode, float* norms_sq, int32_t accumulate,
+                                          void* stream);
 
 /* ---------------------------------------------------------------------------
  * Clip factors.  Paper: Section 2.2, g_bar_i = g_i * min(1, C/||g_i||_2).

@@ -3,6 +3,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -136,6 +137,38 @@ StepPlan plan_step(const dpsgd_layer* layers, int32_t n, int32_t mode) {
   return p;
 }
 
+// Scratch of dpsgd_per_example_norms_multi_noalloc: the per-example norm
+// partials. Each GPU the library runs on holds its own copy from the first
+// use until the process ends. In host code `scratch` only names the symbol;
+// its device address on the current GPU comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[DPSGD_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, resolved once per
+// device; NULL (and *status set) when the runtime cannot provide it.
+void* scratch_on_current_device(int* status) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *status = DPSGD_ERR_HIP;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();   // leave no sticky error for the caller's next call
+      *status = DPSGD_ERR_HIP;
+      return nullptr;
+    }
+    addr[dev] = p;
+  }
+  *status = DPSGD_OK;
+  return addr[dev];
+}
+
 }  // namespace
 }  // namespace dpsgd
 
@@ -183,6 +216,24 @@ int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, i
   if (!aligned16(workspace)) return DPSGD_ERR_INVALID_ARG;
   return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
                       static_cast<float*>(workspace), p.P, p.cols.data(),
+                      static_cast<hipStream_t>(stream));
+}
+
+int dpsgd_per_example_norms_multi_noalloc(const dpsgd_layer* layers, int32_t n_layers,
+                                          int32_t mode, float* norms_sq, int32_t accumulate,
+                                          void* stream) {
+  int st = check_layers(layers, n_layers, true);
+  if (st != DPSGD_OK) return st;
+  if (!valid_mode(mode)) return DPSGD_ERR_UNSUPPORTED;
+  if (!norms_sq) return DPSGD_ERR_INVALID_ARG;
+  const NormPlan p = plan_norms(layers, n_layers, mode);
+  if (p.bytes > DPSGD_NOALLOC_SCRATCH_BYTES) return DPSGD_ERR_WORKSPACE;
+  void* ws = scratch_on_current_device(&st);
+  if (!ws) return st;
+  // Every partial slot [i][col] of the plan is written by exactly one job
+  // before the reduction reads it, so the scratch needs no clearing.
+  return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
+                      static_cast<float*>(ws), p.P, p.cols.data(),
                       static_cast<hipStream_t>(stream));
 }
 

@@ -33,7 +33,8 @@ DPSGD_ERR_HIP = -4
 #: Every symbol the header declares (checked by the CPU test suite).
 EXPORTED = (
     "dpsgd_norms_workspace_bytes", "dpsgd_select_norm_mode", "dpsgd_per_example_norms",
-    "dpsgd_per_example_norms_multi", "dpsgd_clip_factors", "dpsgd_clip_workspace_bytes",
+    "dpsgd_per_example_norms_multi", "dpsgd_per_example_norms_multi_noalloc",
+    "dpsgd_clip_factors", "dpsgd_clip_workspace_bytes",
     "dpsgd_clip_accumulate", "dpsgd_clip_accumulate_multi", "dpsgd_clipped_sum_workspace_bytes",
     "dpsgd_clipped_sum_multi", "dpsgd_add_noise",
     "dpsgd_add_noise_multi", "dpsgd_noise_adamw", "dpsgd_noise_adamw_multi",
@@ -85,6 +86,7 @@ def _declare(lib):
         "dpsgd_select_norm_mode": (i32, [L]),
         "dpsgd_per_example_norms": (ctypes.c_int, [L, i32, vp, i32, vp, sz, vp]),
         "dpsgd_per_example_norms_multi": (ctypes.c_int, [L, i32, i32, vp, i32, vp, sz, vp]),
+        "dpsgd_per_example_norms_multi_noalloc": (ctypes.c_int, [L, i32, i32, vp, i32, vp]),
         "dpsgd_clip_factors": (ctypes.c_int, [vp, i64, f32, vp, vp, vp]),
         "dpsgd_clip_workspace_bytes": (sz, [L, i32]),
         "dpsgd_clip_accumulate": (ctypes.c_int, [L, vp, f32, vp, i32, vp, vp, vp, sz, vp]),
@@ -219,6 +221,18 @@ def dpsgd_per_example_norms_multi(layers, mode, norms_sq, accumulate=False, work
                                             0 if workspace is None else workspace.numel(),
                                             _stream(stream))
     _check("dpsgd_per_example_norms_multi", st)
+
+
+#: Bytes of the scratch array of dpsgd_per_example_norms_multi_noalloc.
+DPSGD_NOALLOC_SCRATCH_BYTES = 8 << 20
+
+
+def dpsgd_per_example_norms_multi_noalloc(layers, mode, norms_sq, accumulate=False, stream=None):
+    load()
+    arr, n = _array(layers)
+    st = _lib.dpsgd_per_example_norms_multi_noalloc(arr, n, mode, _ptr(norms_sq), int(accumulate),
+                                                    _stream(stream))
+    _check("dpsgd_per_example_norms_multi_noalloc", st)
 
 
 def dpsgd_clip_factors(norms_sq, C: float, factors=None, mask=None, stream=None):

@@ -279,3 +279,21 @@ def test_make_layer_requires_a_tensor_id():
     import inspect
     p = inspect.signature(dpsgd.make_layer).parameters["tensor_id"]
     assert p.default is inspect.Parameter.empty
+
+
+def test_noalloc_norms_reject_sizes_beyond_the_scratch(lib):
+    """More partials than the allocation-free call's scratch array holds:
+    refused before the device is touched."""
+    assert dpsgd.DPSGD_NOALLOC_SCRATCH_BYTES == 8 << 20
+    B = (8 << 20) // 4 + 1           # T = 1: one partial per example
+    L = _lay(B=B, T=1, d_in=4, d_out=4)
+    assert dpsgd.dpsgd_norms_workspace_bytes(L, 0) > dpsgd.DPSGD_NOALLOC_SCRATCH_BYTES
+    assert lib.dpsgd_per_example_norms_multi_noalloc(ctypes.byref(L), 1, 0, ctypes.c_void_p(64),
+                                                     0, None) == -3
+    # The usual argument checks come first.
+    assert lib.dpsgd_per_example_norms_multi_noalloc(ctypes.byref(_lay(B=0)), 1, 0,
+                                                     ctypes.c_void_p(64), 0, None) == -1
+    assert lib.dpsgd_per_example_norms_multi_noalloc(ctypes.byref(_lay()), 1, 7,
+                                                     ctypes.c_void_p(64), 0, None) == -2
+    assert lib.dpsgd_per_example_norms_multi_noalloc(ctypes.byref(_lay()), 1, 0, None, 0,
+                                                     None) == -1
