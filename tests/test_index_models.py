@@ -1,0 +1,199 @@
+"""CPU models of kernel index arithmetic, checked before the kernels run.
+
+Each model restates, in NumPy, how a kernel maps its workgroups, lanes and
+copies onto the data, and checks on the CPU that every access stays inside
+its buffer and that the mapped computation gives the intended product on
+ragged shapes. They share no code with the library (they restate the
+mapping), so a change to a kernel's indexing must be mirrored here.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+# ---------------------------------------------------------------- helpers
+
+
+def xcd_two_class_index(bid, nwg, n_first):
+    """Workgroup bid -> logical job: every XCD (bid % 8) gets an even share of
+    the first n_first jobs as one contiguous range, then of the rest."""
+    xcd, idx = bid & 7, bid >> 3
+    per, rem = nwg >> 3, nwg & 7
+    fper, frem = n_first >> 3, n_first & 7
+    f_cnt = fper + (1 if xcd < frem else 0)
+    f_begin = xcd * fper + (xcd if xcd < frem else frem)
+    if idx < f_cnt:
+        return f_begin + idx
+    begin = xcd * per + (xcd if xcd < rem else rem)
+    return n_first + (begin - f_begin) + (idx - f_cnt)
+
+
+@pytest.mark.parametrize("nwg,n_first", [(576, 512), (640, 512), (1, 0), (7, 3), (4096, 4096),
+                                         (1000, 0), (9, 9), (513, 256)])
+def test_xcd_two_class_index_is_a_permutation(nwg, n_first):
+    jobs = [xcd_two_class_index(b, nwg, n_first) for b in range(nwg)]
+    assert sorted(jobs) == list(range(nwg))
+
+
+# ------------------------------------- k-major float32 kernel (tgemm_k32_kernel)
+
+K32_ROWS = 32                               # k rows per slice
+K32_STAGE = K32_ROWS * (64 + 256)           # floats of the largest slice (64 x 256 tile)
+K32_MAX_COPIES = K32_STAGE // 256 // 4      # 1 KB copies per wave
+
+
+def k32_tile(M):
+    return (64, 256) if M <= 64 else (128, 128)
+
+
+def k32_slice(G, A, M, N, tmi, tni, q, sumsq):
+    """One slice q of tile (tmi, tni) through the kernel's copies and operand
+    reads. Returns the tile's 32-row product (and checks every access)."""
+    TM, TN = k32_tile(M)
+    nm, ncopy = TM // 8, (TM + TN) // 8
+    assert ncopy <= 4 * K32_MAX_COPIES
+    lds = np.zeros(K32_STAGE, np.float64) if sumsq else np.full(K32_STAGE, np.nan)
+    for wave in range(4):
+        for p in range(K32_MAX_COPIES):
+            c = wave + 4 * p
+            if c >= ncopy:
+                continue
+            mside = c < nm
+            W, R, X = (TM, M, G) if mside else (TN, N, A)
+            lane = np.arange(64)
+            f = 256 * (c if mside else c - nm) + 4 * lane
+            k, pc = f // W, f & (W - 1)
+            col = (tmi * TM if mside else tni * TN) + ((pc + W - 32 * (k & 1)) & (W - 1))
+            voff = k * R * 4 + np.minimum(col, R - 4) * 4
+            assert np.all(voff < 2 ** 32) and np.all(k < K32_ROWS)
+            byte0 = q * K32_ROWS * R * 4 + voff
+            assert np.all(byte0 + 16 <= X.size * 4) and np.all(byte0 % 16 == 0)
+            dst = 1024 * c + 16 * lane
+            assert np.all(dst + 16 <= K32_STAGE * 4)
+            for ln in range(64):
+                if sumsq and col[ln] >= R:
+                    continue          # the norm variant leaves these words at zero
+                b0 = byte0[ln] // 4
+                lds[dst[ln] // 4: dst[ln] // 4 + 4] = X.reshape(-1)[b0:b0 + 4]
+    wc = TN // 64
+    out = np.zeros((TM, TN))
+    for wave in range(4):
+        wm, wn = wave // wc, wave % wc
+        for a in range(2):
+            for b in range(2):
+                D = np.zeros((32, 32))
+                lane = np.arange(64)
+                h, c32 = lane >> 5, lane & 31
+                oa = h * TM + ((wm * 64 + 32 * a + 32 * h) & (TM - 1)) + c32
+                ob = K32_ROWS * TM + h * TN + ((wn * 64 + 32 * b + 32 * h) & (TN - 1)) + c32
+                for kp in range(K32_ROWS // 2):
+                    ia, ib = oa + 2 * kp * TM, ob + 2 * kp * TN
+                    assert np.all(ia < K32_ROWS * TM)
+                    assert np.all((K32_ROWS * TM <= ib) & (ib < K32_ROWS * (TM + TN)))
+                    Aop = np.zeros((32, 2))
+                    Bop = np.zeros((2, 32))
+                    Aop[c32, h] = lds[ia]
+                    Bop[h, c32] = lds[ib]
+                    D += Aop @ Bop
+                out[wm * 64 + 32 * a: wm * 64 + 32 * a + 32,
+                    wn * 64 + 32 * b: wn * 64 + 32 * b + 32] = D
+    return out
+
+
+@pytest.mark.parametrize("M,N", [(64, 576), (64, 16), (128, 1152), (12, 100), (100, 36),
+                                 (64, 144), (132, 260), (256, 2304)])
+def test_k32_copies_and_reads_give_the_tile_product(M, N):
+    """Ragged widths, both tile shapes: the clip variant's tile equals
+    G_sliceᵀ A_slice on its valid part, and the norm variant's tile (copies
+    past the edge skipped, words left at zero) has exactly the valid part's
+    sum of squares."""
+    T, B = 64, 2
+    rng = np.random.default_rng(M * 1000 + N)
+    G = rng.standard_normal((B * T, M)).astype(np.float32)
+    A = rng.standard_normal((B * T, N)).astype(np.float32)
+    TM, TN = k32_tile(M)
+    tiles = [(tmi, tni) for tmi in range(-(-M // TM)) for tni in range(-(-N // TN))]
+    if len(tiles) > 6:
+        tiles = tiles[:3] + tiles[-3:]
+    for tmi, tni in tiles:
+        for q in (0, B * T // K32_ROWS - 1):
+            rows = slice(q * K32_ROWS, (q + 1) * K32_ROWS)
+            ref = G[rows].astype(np.float64).T @ A[rows].astype(np.float64)
+            m0, n0 = tmi * TM, tni * TN
+            mv, nv = min(TM, M - m0), min(TN, N - n0)
+            out = k32_slice(G, A, M, N, tmi, tni, q, sumsq=False)
+            assert not np.isnan(out[:mv, :nv]).any()
+            np.testing.assert_allclose(out[:mv, :nv], ref[m0:m0 + mv, n0:n0 + nv], atol=1e-9)
+            sq = k32_slice(G, A, M, N, tmi, tni, q, sumsq=True)
+            assert math.isclose(float(np.sum(sq * sq)),
+                                float(np.sum(ref[m0:m0 + mv, n0:n0 + nv] ** 2)), rel_tol=1e-12)
+
+
+def test_k32_every_wave_has_copies():
+    for TM, TN in ((64, 256), (128, 128)):
+        nc = (TM + TN) // 8
+        assert nc * 1024 <= K32_STAGE * 4
+        for wave in range(4):
+            assert sum(1 for p in range(K32_MAX_COPIES) if wave + 4 * p < nc) >= 4
+
+
+# ------------------------------------------- float32 Gram form (gram64_kernel)
+
+G64_COLS = 64
+
+
+def g64_word(t, k):
+    """Word of (row t, column k) in a slice: row t rotated by t 16-byte units."""
+    return t * G64_COLS + 4 * (((k >> 2) + t) & 15) + (k & 3)
+
+
+@pytest.mark.parametrize("T,d_in,d_out", [(64, 128, 64), (37, 64, 128), (2, 64, 64), (63, 192, 64)])
+def test_gram64_copies_and_reads_give_the_norm(T, d_in, d_out):
+    """Example ex of B: the slices' copies (rows past T never copied, slots
+    zeroed) and the MFMA operand reads give Σ (A Aᵀ)∘(G Gᵀ) = ||Gᵀ A||²."""
+    B, ex = 2, 1
+    rng = np.random.default_rng(T + d_in)
+    A = rng.standard_normal((B * T, d_in)).astype(np.float32)
+    G = rng.standard_normal((B * T, d_out)).astype(np.float32)
+    na, ns = d_in // G64_COLS, d_in // G64_COLS + d_out // G64_COLS
+    accA, accG = np.zeros((64, 64)), np.zeros((64, 64))
+    assert all(g64_word(t, k) < 64 * 64 for t in range(64) for k in range(64))
+    assert len({g64_word(t, k) for t in range(64) for k in range(64)}) == 64 * 64
+    for s in range(ns):
+        lds = np.zeros(64 * 64)
+        is_a = s < na
+        X, d = (A, d_in) if is_a else (G, d_out)
+        col0 = (s if is_a else s - na) * G64_COLS
+        base = ex * T * d + col0
+        for wave in range(4):
+            for p in range(4):
+                c = wave + 4 * p
+                for lane in range(64):
+                    t, u = 4 * c + (lane >> 4), lane & 15
+                    col = 4 * ((u - t) & 15)
+                    voff = t * d * 4 + col * 4
+                    assert voff < 2 ** 32
+                    if t >= T:
+                        continue
+                    f = base + voff // 4
+                    assert f + 4 <= X.size and col0 + col + 4 <= d
+                    dst = 1024 * c + 16 * lane
+                    assert dst + 16 <= 64 * 64 * 4
+                    lds[dst // 4: dst // 4 + 4] = X.reshape(-1)[f:f + 4]
+        acc = accA if is_a else accG
+        for wave in range(4):
+            bm, bn = wave >> 1, wave & 1
+            for kp in range(32):
+                Aop, Bop = np.zeros((32, 2)), np.zeros((2, 32))
+                for lane in range(64):
+                    h, c32 = lane >> 5, lane & 31
+                    k = 2 * kp + h
+                    Aop[c32, h] = lds[g64_word(32 * bm + c32, k)]
+                    Bop[h, c32] = lds[g64_word(32 * bn + c32, k)]
+                acc[32 * bm:32 * bm + 32, 32 * bn:32 * bn + 32] += Aop @ Bop
+    got = float((accA * accG).sum())
+    Ai = A[ex * T:(ex + 1) * T].astype(np.float64)
+    Gi = G[ex * T:(ex + 1) * T].astype(np.float64)
+    ref = float(((Gi.T @ Ai) ** 2).sum())
+    assert math.isclose(got, ref, rel_tol=1e-9)
