@@ -94,21 +94,27 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
   constexpr int G = 64 / R;   // rows per narrow load
   constexpr int U = 16 / G > 1 ? 16 / G : 1;   // narrow loads per iteration
   constexpr int RI = G * U;   // rows per iteration: 16 wide loads in flight per lane
-  const uint32_t job = blockIdx.x * kSkWaves + (threadIdx.x >> 6);
+  // The wave index is read as a scalar, so the layer descriptor below is
+  // read with scalar loads, and its fields are copied into registers before
+  // the row loop (a field read inside the loop's conditional loads would be
+  // reloaded there, each reload waiting for every load in flight).
+  const uint32_t job = blockIdx.x * kSkWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (job >= args.jobs) return;   // whole waves
   const int lane = threadIdx.x & 63;
   const SkEntry& E = args.L[sk_find_layer(args, job)];
+  const int64_t d_w = E.d_w, r = E.r;
+  const int T = E.T;
   const uint32_t w = job - E.job_begin;
   const int chunk = (int)(w % (uint32_t)E.chunks);
   const uint32_t rest = w / (uint32_t)E.chunks;
   const int64_t i = rest % (uint32_t)args.B;
   const int s = (int)(rest / (uint32_t)args.B);
-  const int t0 = (int)((int64_t)E.T * s / E.splits);
-  const int t1 = (int)((int64_t)E.T * (s + 1) / E.splits);
+  const int t0 = (int)((int64_t)T * s / E.splits);
+  const int t1 = (int)((int64_t)T * (s + 1) / E.splits);
   const int col = (chunk * 64 + lane) * V;
-  const bool col_ok = col < E.d_w;
-  const TIn* W = static_cast<const TIn*>(E.wide) + i * E.T * (int64_t)E.d_w + (col_ok ? col : 0);
-  const TIn* Nr = static_cast<const TIn*>(E.narrow) + i * E.T * (int64_t)E.r;
+  const bool col_ok = col < d_w;
+  const TIn* W = static_cast<const TIn*>(E.wide) + i * T * d_w + (col_ok ? col : 0);
+  const TIn* Nr = static_cast<const TIn*>(E.narrow) + i * T * r;
   const int nrow = lane / R, ncol = lane % R;
 
   float acc[R][V];
@@ -123,14 +129,14 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
 #pragma unroll
     for (int uu = 0; uu < U; ++uu) {
       nv[uu] = 0.f;
-      if (ncol < E.r && uu * G + nrow < rows)
-        nv[uu] = sk_load(Nr + (int64_t)(tg + uu * G + nrow) * E.r + ncol);
+      if (ncol < r && uu * G + nrow < rows)
+        nv[uu] = sk_load(Nr + (int64_t)(tg + uu * G + nrow) * r + ncol);
     }
     Raw wv[RI];
 #pragma unroll
     for (int u = 0; u < RI; ++u) {
       wv[u] = Raw{};
-      if (u < rows && col_ok) wv[u] = *reinterpret_cast<const Raw*>(W + (int64_t)(tg + u) * E.d_w);
+      if (u < rows && col_ok) wv[u] = *reinterpret_cast<const Raw*>(W + (int64_t)(tg + u) * d_w);
     }
 #pragma unroll
     for (int u = 0; u < RI; ++u) {
@@ -179,6 +185,134 @@ __global__ __launch_bounds__(kThreads) void skinny_grad_kernel(SkArgs args) {
 #pragma unroll
         for (int j = 0; j < R; ++j)
           if (j < E.r) dst[(int64_t)(col + v) * E.r + j] = acc[j][v];
+    }
+  }
+  if (E.splits == 1) {
+    sq = wave_sum(sq);
+    if (lane == 0) args.partials[i * args.P + E.partial_col + chunk] = sq;
+  }
+}
+
+// MFMA form for bfloat16 inputs whose wide side is a multiple of 8. The
+// per-example gradient is the product N^T W over the rows (N the narrow
+// side, W the wide side), which v_mfma_f32_16x16x32_bf16 takes 32 rows at a
+// time (bf16 products are exact in float32, sums accumulate in float32, as on
+// the VALU path). One wave owns 128 wide columns and one row range of one
+// example. For rows t .. t + 31, lane l loads the 8 x 8 block of W at rows
+// t + 8 (l / 16) .. +7 and columns 8 (l % 16) .. +7 (eight 16-byte loads)
+// and transposes it in registers, so that operand j holds column
+// 8 (l % 16) + j at those eight rows; its narrow operand holds column l % 16
+// of N at the same rows (zero past r). MFMA j then gives g rows 0 .. 15 for
+// the wide columns 8 n + j, n = 0 .. 15. Narrow columns past r and rows past
+// the range are zero on input, so their outputs are zero. The next 32 rows'
+// loads are issued before the current block is multiplied.
+constexpr int kSkmCols = 128;   // wide columns per wave (and per norm chunk)
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t skm_bits(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  return __builtin_bit_cast(bf16x8_t, (u32x4_t{w0, w1, w2, w3}));
+}
+
+__global__ __launch_bounds__(kThreads) void skinny_mfma_kernel(SkArgs args) {
+  // Scalar wave index and descriptor fields in registers, as in
+  // skinny_grad_kernel.
+  const uint32_t job = blockIdx.x * kSkWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (job >= args.jobs) return;   // whole waves
+  const int lane = threadIdx.x & 63;
+  const SkEntry& E = args.L[sk_find_layer(args, job)];
+  const int64_t d_w = E.d_w, r = E.r;
+  const int T = E.T;
+  const uint32_t w = job - E.job_begin;
+  const int chunk = (int)(w % (uint32_t)E.chunks);
+  const uint32_t rest = w / (uint32_t)E.chunks;
+  const int64_t i = rest % (uint32_t)args.B;
+  const int s = (int)(rest / (uint32_t)args.B);
+  const int t0 = (int)((int64_t)T * s / E.splits);
+  const int t1 = (int)((int64_t)T * (s + 1) / E.splits);
+  const int g = lane >> 4, cl = lane & 15;
+  const int col = chunk * kSkmCols + 8 * cl;
+  const bool col_ok = col < d_w;   // d_w % 8 == 0: all eight columns or none
+  const uint16_t* W = static_cast<const uint16_t*>(E.wide) + i * T * d_w + (col_ok ? col : 0);
+  const uint16_t* Nr = static_cast<const uint16_t*>(E.narrow) + i * T * r;
+  const bool n_ok = cl < r;
+
+  f32x4_t acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  uint4 wv[8];
+  uint32_t nv[8];
+  auto load = [&](int tg) {
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const int t = tg + 8 * g + kk;
+      wv[kk] = uint4{0u, 0u, 0u, 0u};
+      nv[kk] = 0u;
+      if (t < t1) {
+        if (col_ok) wv[kk] = *reinterpret_cast<const uint4*>(W + (int64_t)t * d_w);
+        if (n_ok) nv[kk] = Nr[(int64_t)t * r + cl];
+      }
+    }
+  };
+  if (t0 < t1) load(t0);
+  for (int tg = t0; tg < t1; tg += 32) {
+    // Transpose the 8 x 8 block: word q of operand j packs rows 2q and
+    // 2q + 1 of column j (the low halves of word j / 2 for even j, the high
+    // halves for odd j).
+    uint32_t c[8][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint4 x = wv[2 * q], y = wv[2 * q + 1];
+      c[0][q] = __builtin_amdgcn_perm(y.x, x.x, 0x05040100u);
+      c[1][q] = __builtin_amdgcn_perm(y.x, x.x, 0x07060302u);
+      c[2][q] = __builtin_amdgcn_perm(y.y, x.y, 0x05040100u);
+      c[3][q] = __builtin_amdgcn_perm(y.y, x.y, 0x07060302u);
+      c[4][q] = __builtin_amdgcn_perm(y.z, x.z, 0x05040100u);
+      c[5][q] = __builtin_amdgcn_perm(y.z, x.z, 0x07060302u);
+      c[6][q] = __builtin_amdgcn_perm(y.w, x.w, 0x05040100u);
+      c[7][q] = __builtin_amdgcn_perm(y.w, x.w, 0x07060302u);
+    }
+    const bf16x8_t a = skm_bits(nv[0] | (nv[1] << 16), nv[2] | (nv[3] << 16),
+                                nv[4] | (nv[5] << 16), nv[6] | (nv[7] << 16));
+    if (tg + 32 < t1) load(tg + 32);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          a, skm_bits(c[j][0], c[j][1], c[j][2], c[j][3]), acc[j], 0, 0, 0);
+  }
+
+  // Output v of MFMA j in lane l: g row m = 4 (l / 16) + v, wide column
+  // chunk * 128 + 8 (l % 16) + j.
+  float sq = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sq = fmaf(acc[j][v], acc[j][v], sq);
+  float* dst = E.store + ((int64_t)s * args.B + i) * ((int64_t)E.d_w * E.r);
+  const int m0 = 4 * g;
+  if (col_ok && m0 < E.r) {
+    if (!E.narrow_is_a) {
+      // g is [r][d_w]: row m holds this lane's eight columns contiguously.
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (m0 + v < E.r) {
+          float* p = dst + (int64_t)(m0 + v) * E.d_w + col;
+          *reinterpret_cast<float4*>(p) = make_float4(acc[0][v], acc[1][v], acc[2][v], acc[3][v]);
+          *reinterpret_cast<float4*>(p + 4) = make_float4(acc[4][v], acc[5][v], acc[6][v], acc[7][v]);
+        }
+    } else if ((E.r & 3) == 0) {
+      // g is [d_w][r]: rows m0 .. m0 + 3 of column c are four contiguous floats.
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<float4*>(dst + (int64_t)(col + j) * E.r + m0) =
+            make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (m0 + v < E.r) dst[(int64_t)(col + j) * E.r + m0 + v] = acc[j][v];
     }
   }
   if (E.splits == 1) {
@@ -333,7 +467,12 @@ bool skinny_ok(const dpsgd_layer& L) {
   return 4.0 * sk_grad_bytes(L) <= sk_input_bytes(L);
 }
 
-int64_t skinny_chunks(const dpsgd_layer& L) { return ceil_div(sk_wide(L), 64 * sk_vec(L)); }
+// bf16 layers whose wide side is a multiple of 8 take the MFMA kernel.
+bool sk_mfma(const dpsgd_layer& L) { return L.dtype == DPSGD_BF16 && sk_wide(L) % 8 == 0; }
+
+int64_t skinny_chunks(const dpsgd_layer& L) {
+  return ceil_div(sk_wide(L), sk_mfma(L) ? kSkmCols : 64 * sk_vec(L));
+}
 
 void plan_skinny(const dpsgd_layer* layers, const int* idx, int n, int cus, int64_t* splits) {
   int64_t base = 0;
@@ -357,21 +496,24 @@ size_t skinny_store_bytes(const dpsgd_layer& L, int64_t splits) {
 }
 
 // One pair of launches (grad, then finish when a layer has several row
-// ranges) per class of padded rank R and per kMaxLayersPerLaunch layers; the
-// class fixes the kernel's R and V.
+// ranges) per class and per kMaxLayersPerLaunch layers: the MFMA class
+// (class 0), then the VALU kernel's classes of padded rank R, which fix its R
+// and V.
 int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                         const int64_t* splits, float* const* stores, float* partials, int64_t P,
                         hipStream_t stream) {
   if (n <= 0) return DPSGD_OK;
   const bool bf16 = layers[idx[0]].dtype == DPSGD_BF16;
-  for (int R : {4, 8, 16}) {
+  for (int R : {0, 4, 8, 16}) {
     int pos[kMaxLayersPerLaunch];
     int k0 = 0;
     while (k0 < n) {
       // The next up to kMaxLayersPerLaunch layers of this class.
       int m = 0;
-      for (; k0 < n && m < kMaxLayersPerLaunch; ++k0)
-        if (sk_rpad(layers[idx[k0]]) == R) pos[m++] = k0;
+      for (; k0 < n && m < kMaxLayersPerLaunch; ++k0) {
+        const dpsgd_layer& L = layers[idx[k0]];
+        if ((sk_mfma(L) ? 0 : sk_rpad(L)) == R) pos[m++] = k0;
+      }
       if (m == 0) break;
       SkArgs ga{}, fa{};
       ga.n = fa.n = m;
@@ -405,7 +547,10 @@ int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const 
       if (gjobs > 0x7FFFFFFF || fjobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
       ga.jobs = (uint32_t)gjobs;
       fa.jobs = (uint32_t)fjobs;
-      if (bf16) {
+      if (R == 0) {
+        hipLaunchKernelGGL(skinny_mfma_kernel, dim3((ga.jobs + kSkWaves - 1) / kSkWaves),
+                           dim3(kThreads), 0, stream, ga);
+      } else if (bf16) {
         if (R == 4) launch_grad<uint16_t, 4, 4>(ga, stream);
         else if (R == 8) launch_grad<uint16_t, 8, 4>(ga, stream);
         else launch_grad<uint16_t, 16, 4>(ga, stream);
@@ -416,7 +561,12 @@ int launch_skinny_norms(const dpsgd_layer* layers, const int* idx, int n, const 
       }
       if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
       if (fjobs > 0) {
-        hipLaunchKernelGGL(skinny_finish_kernel<4>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
+        // Chunks of 64 V wide columns: 128 for the MFMA class, 256 otherwise.
+        if (R == 0)
+          hipLaunchKernelGGL(skinny_finish_kernel<kSkmCols / 64>, dim3(fa.jobs), dim3(kThreads), 0,
+                             stream, fa);
+        else
+          hipLaunchKernelGGL(skinny_finish_kernel<4>, dim3(fa.jobs), dim3(kThreads), 0, stream, fa);
         if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
       }
     }

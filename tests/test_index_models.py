@@ -197,3 +197,105 @@ def test_gram64_copies_and_reads_give_the_norm(T, d_in, d_out):
     Gi = G[ex * T:(ex + 1) * T].astype(np.float64)
     ref = float(((Gi.T @ Ai) ** 2).sum())
     assert math.isclose(got, ref, rel_tol=1e-9)
+
+
+# ------------------------------- stored per-example gradient, MFMA form (bf16)
+
+def v_perm(src0, src1, sel):
+    """v_perm_b32: byte i of the result is byte (sel >> 8 i) & 0xFF of the
+    eight bytes {src1 (bytes 0-3), src0 (bytes 4-7)}."""
+    pool = int(src1) | (int(src0) << 32)
+    out = 0
+    for i in range(4):
+        b = (sel >> (8 * i)) & 0xFF
+        out |= ((pool >> (8 * b)) & 0xFF) << (8 * i)
+    return out
+
+
+def bf16_values(words):
+    """uint32 words -> their two bf16 halves as floats (low half first)."""
+    out = []
+    for wd in words:
+        for h in (wd & 0xFFFF, wd >> 16):
+            out.append(float(np.array([h << 16], np.uint32).view(np.float32)[0]))
+    return out
+
+
+def mfma_16x16x32(a_lane, b_lane, acc):
+    """v_mfma_f32_16x16x32_bf16: lane l supplies A[l % 16][8 (l // 16) + e]
+    and B[8 (l // 16) + e][l % 16] (e = 0..7); output v of lane l is
+    D[4 (l // 16) + v][l % 16]."""
+    A = np.zeros((16, 32))
+    Bm = np.zeros((32, 16))
+    for ln in range(64):
+        A[ln % 16, 8 * (ln // 16): 8 * (ln // 16) + 8] = a_lane[ln]
+        Bm[8 * (ln // 16): 8 * (ln // 16) + 8, ln % 16] = b_lane[ln]
+    D = A @ Bm
+    for ln in range(64):
+        for v in range(4):
+            acc[ln][v] += D[4 * (ln // 16) + v, ln % 16]
+
+
+@pytest.mark.parametrize("T,d_w,r,narrow_is_a,chunk,t0,t1", [
+    (37, 256, 16, True, 1, 0, 37), (64, 384, 5, False, 2, 8, 45), (29, 128, 4, True, 0, 3, 29),
+    (16, 136, 16, False, 1, 0, 16)])
+def test_skinny_mfma_lanes_form_the_gradient(T, d_w, r, narrow_is_a, chunk, t0, t1):
+    """One wave of the MFMA stored-gradient kernel, bit by bit on bf16 data:
+    its loads (wide columns past d_w, narrow columns past r and rows past the
+    range read as zero), the in-register 8 x 8 transposes, the MFMAs and the
+    stores give g = N^T W over rows [t0, t1) of the chunk's 128 columns, in
+    the layout of G^T A."""
+    rng = np.random.default_rng(T * d_w + r)
+    to_bf16 = lambda x: (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint32)
+    Nb = to_bf16(rng.standard_normal((T, r)))
+    Wb = to_bf16(rng.standard_normal((T, d_w)))
+    f = lambda b: (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    acc = np.zeros((8, 64, 4))
+    for tg in range(t0, t1, 32):
+        a_lane, b_lanes = [], [[] for _ in range(8)]
+        for ln in range(64):
+            g, cl = ln // 16, ln % 16
+            col = chunk * 128 + 8 * cl
+            rows = []      # the lane's eight 16-byte loads, as four uint32 words each
+            nv = []
+            for kk in range(8):
+                t = tg + 8 * g + kk
+                words = [0, 0, 0, 0]
+                n = 0
+                if t < t1:
+                    if col < d_w:
+                        assert col + 8 <= d_w
+                        e = Wb[t, col:col + 8]
+                        words = [int(e[2 * q]) | (int(e[2 * q + 1]) << 16) for q in range(4)]
+                    if cl < r:
+                        n = int(Nb[t, cl])
+                rows.append(words)
+                nv.append(n)
+            a_lane.append(bf16_values([nv[2 * q] | (nv[2 * q + 1] << 16) for q in range(4)]))
+            for j in range(8):
+                sel = 0x05040100 if j % 2 == 0 else 0x07060302
+                wq = [v_perm(rows[2 * q + 1][j // 2], rows[2 * q][j // 2], sel) for q in range(4)]
+                b_lanes[j].append(bf16_values(wq))
+        for j in range(8):
+            mfma_16x16x32(a_lane, b_lanes[j], acc[j])
+    got = np.zeros((r, d_w)) if not narrow_is_a else np.zeros((d_w, r))
+    written = np.zeros_like(got, dtype=bool)
+    for ln in range(64):
+        m0, col = 4 * (ln // 16), chunk * 128 + 8 * (ln % 16)
+        if col >= d_w or m0 >= r:
+            continue
+        for j in range(8):
+            for v in range(4):
+                if m0 + v < r:
+                    idx = (col + j, m0 + v) if narrow_is_a else (m0 + v, col + j)
+                    got[idx] = acc[j][ln][v]
+                    written[idx] = True
+    ref = f(Nb[t0:t1]).T @ f(Wb[t0:t1])           # [r][d_w]
+    if narrow_is_a:
+        ref = ref.T
+    c0, c1 = chunk * 128, min(d_w, chunk * 128 + 128)
+    sl = (slice(c0, c1), slice(None)) if narrow_is_a else (slice(None), slice(c0, c1))
+    assert written[sl].all() and written.sum() == written[sl].size
+    np.testing.assert_allclose(got[sl], ref[sl], rtol=1e-12, atol=1e-12)
+    # The wave's norm partial (every output, zeros included) is the chunk's.
+    assert math.isclose(float(np.sum(acc ** 2)), float(np.sum(ref[sl] ** 2)), rel_tol=1e-12)
