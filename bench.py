@@ -35,9 +35,9 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 METRIC = "DP-SGD clipped+noised grad throughput: examples/s per layer; % MFMA peak"
 
-# HBM bytes per launch of the clip GEMM measured with rocprofv3 counters; valid
-# only for the kernel sources they were taken with.
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "clip_gemm_c5_traffic.txt")
+# HBM bytes per launch of the clip GEMM measured with rocprofv3 counters, one
+# record per workload; valid only for the kernel sources they were taken with.
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "clip_gemm_{workload}_traffic.txt")
 GEMM_SOURCES = [os.path.join(HERE, "paper_2609_20532_amd", "csrc", f)
                 for f in ("gemm_wide.hip", "gemm_tr.hip", "gemm.hip", "lds_dma.h", "mma.h",
                           "common.h")]
@@ -80,7 +80,7 @@ def measured_traffic(workload: str):
     """HBM bytes (fetch + write) of one clip GEMM launch, from the counter file,
     or None when it is missing, for another workload or for other sources."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(TRAFFIC_FILE.format(workload=workload)) as fh:
             rec = dict(line.split(None, 1) for line in fh if line.strip() and not line.startswith("#"))
     except OSError:
         return None
