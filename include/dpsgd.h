@@ -103,7 +103,11 @@ typedef struct dpsgd_layer {
  *   norms_sq  float32 [B], device.
  *   workspace device scratch of at least dpsgd_norms_workspace_bytes(...)
  *             bytes, 16-byte aligned (DPSGD_ERR_INVALID_ARG otherwise); its
- *             contents on entry do not matter and are clobbered.
+ *             contents on entry do not matter and are clobbered. It holds
+ *             per-example partials and, when a bf16 layer with T > 256 and
+ *             widths that are multiples of 64 runs the Gram form, a park
+ *             area of 256 KB per workgroup of that kernel (at most 512
+ *             workgroups: 128 MB).
  * T = 1 layers always use the closed form ||a||^2 ||g||^2 whatever the mode.
  * ------------------------------------------------------------------------- */
 size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode);
@@ -128,19 +132,22 @@ int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, i
  * allocate device memory: code under HIP graph capture, tight serving loops,
  * harnesses that forbid allocation.
  *
- * The operation, arguments and results of dpsgd_per_example_norms_multi
- * (bit for bit: the same kernels run), with the per-example partials kept
- * in a scratch array of DPSGD_NOALLOC_SCRATCH_BYTES bytes that the library
- * holds in the memory of each GPU it runs on, from the first call on that
- * GPU until the process ends. The call allocates nothing.
+ * The operation, arguments and results of dpsgd_per_example_norms_multi,
+ * with the per-example partials kept in a scratch array of
+ * DPSGD_NOALLOC_SCRATCH_BYTES bytes that the library holds in the memory of
+ * each GPU it runs on, from the first call on that GPU until the process
+ * ends. The call allocates nothing. Results equal the workspace call's bit
+ * for bit (the same kernels run), except for bf16 Gram-form layers with
+ * T > 256: the workspace call runs them on 256-row tiles, whose park area
+ * the array does not hold, this call on 128-row tiles, so their norms agree
+ * to float32 rounding.
  *  - Runs on the current device (hipSetDevice), whose stream `stream` must be.
  *    The first call on a device resolves the array's address there (no
  *    stream work); make it before capturing a graph that contains the call.
  *  - DPSGD_ERR_WORKSPACE when the layers need more partial storage than the
- *    array holds (dpsgd_norms_workspace_bytes(layers, n, mode) >
- *    DPSGD_NOALLOC_SCRATCH_BYTES, i.e. about 2M partials: B times the sum
- *    over layers of the partials per example); checked before anything else
- *    touches the device. DPSGD_ERR_HIP when the runtime cannot give the
+ *    array holds (about 2M float partials: B times the sum over layers of
+ *    the partials per example, a T > 256 Gram-form layer counting its
+ *    128-row tile pairs); checked before anything else touches the device. DPSGD_ERR_HIP when the runtime cannot give the
  *    array's address on the current device. Other errors as in
  *    dpsgd_per_example_norms_multi.
  *  - Every call on one GPU uses that GPU's one array, which keeps the last

@@ -49,23 +49,45 @@ int check_layers(const dpsgd_layer* layers, int32_t n, bool data) {
   return DPSGD_OK;
 }
 
+// Norm workspace: partials [B][P], then (when a layer runs the Gram form on
+// 256-row tiles) the park area of those tiles.
 struct NormPlan {
   std::vector<NormForm> forms;
   std::vector<int64_t> cols;
   int64_t P = 0;
+  size_t park_off = 0;
   size_t bytes = 0;
+  float* park(void* ws) const {
+    return park_off == bytes ? nullptr : reinterpret_cast<float*>(static_cast<char*>(ws) + park_off);
+  }
 };
 
-NormPlan plan_norms(const dpsgd_layer* layers, int32_t n, int32_t mode) {
+// Form of layer l in a plan: the resolved form, with the Gram form moved to
+// 256-row tiles where the layer qualifies and a park area is allowed.
+NormForm planned_form(const dpsgd_layer& L, NormForm f, bool park_ok) {
+  return f == FORM_GHOST && park_ok && ghost256_ok(L) ? FORM_GHOST256 : f;
+}
+
+// Fills cols, P, park_off and bytes from forms.
+void finish_norm_plan(const dpsgd_layer* layers, int32_t n, NormPlan* p) {
+  int64_t jobs256 = 0;
+  p->P = 0;
+  for (int32_t l = 0; l < n; ++l) {
+    p->cols[l] = p->P;
+    p->P += norm_partials_per_example(layers[l], p->forms[l]);
+    if (p->forms[l] == FORM_GHOST256) jobs256 += layers[l].B * ghost256_pairs(layers[l]);
+  }
+  p->park_off = round_up((size_t)layers[0].B * (size_t)p->P * sizeof(float), 256);
+  p->bytes = p->park_off + (jobs256 > 0 ? ghost256_park_bytes(jobs256) : 0);
+}
+
+NormPlan plan_norms(const dpsgd_layer* layers, int32_t n, int32_t mode, bool park_ok) {
   NormPlan p;
   p.forms.resize(n);
   p.cols.resize(n);
-  for (int32_t l = 0; l < n; ++l) {
-    p.forms[l] = resolve_norm_form(layers[l], mode);
-    p.cols[l] = p.P;
-    p.P += norm_partials_per_example(layers[l], p.forms[l]);
-  }
-  p.bytes = round_up((size_t)layers[0].B * (size_t)p.P * sizeof(float), 256);
+  for (int32_t l = 0; l < n; ++l)
+    p.forms[l] = planned_form(layers[l], resolve_norm_form(layers[l], mode), park_ok);
+  finish_norm_plan(layers, n, &p);
   return p;
 }
 
@@ -112,13 +134,12 @@ StepPlan plan_step(const dpsgd_layer* layers, int32_t n, int32_t mode) {
   p.norms.cols.resize(n);
   for (int32_t l = 0; l < n; ++l) {
     const bool stored = mode != DPSGD_NORM_GHOST && skinny_ok(layers[l]);
-    p.norms.forms[l] = stored ? FORM_STORED : resolve_norm_form(layers[l], mode);
-    p.norms.cols[l] = p.norms.P;
-    p.norms.P += norm_partials_per_example(layers[l], p.norms.forms[l]);
+    p.norms.forms[l] =
+        stored ? FORM_STORED : planned_form(layers[l], resolve_norm_form(layers[l], mode), true);
     (stored ? p.stored : p.other).push_back(l);
   }
+  finish_norm_plan(layers, n, &p.norms);
   const int64_t B = layers[0].B;
-  p.norms.bytes = round_up((size_t)B * (size_t)p.norms.P * sizeof(float), 256);
   for (int l : p.other) p.other_layers.push_back(layers[l]);
   const size_t clip = p.other.empty()
                           ? round_up((size_t)B * sizeof(float), kFactorBytesAlign)
@@ -191,7 +212,7 @@ int dpsgd_version(void) { return 1; }
 
 size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode) {
   if (check_layers(layers, n_layers, false) != DPSGD_OK || !valid_mode(mode)) return 0;
-  return plan_norms(layers, n_layers, mode).bytes;
+  return plan_norms(layers, n_layers, mode, true).bytes;
 }
 
 int32_t dpsgd_select_norm_mode(const dpsgd_layer* layer) {
@@ -211,11 +232,11 @@ int dpsgd_per_example_norms_multi(const dpsgd_layer* layers, int32_t n_layers, i
   if (st != DPSGD_OK) return st;
   if (!valid_mode(mode)) return DPSGD_ERR_UNSUPPORTED;
   if (!norms_sq) return DPSGD_ERR_INVALID_ARG;
-  const NormPlan p = plan_norms(layers, n_layers, mode);
+  const NormPlan p = plan_norms(layers, n_layers, mode, true);
   if (!workspace || workspace_bytes < p.bytes) return DPSGD_ERR_WORKSPACE;
   if (!aligned16(workspace)) return DPSGD_ERR_INVALID_ARG;
   return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
-                      static_cast<float*>(workspace), p.P, p.cols.data(),
+                      static_cast<float*>(workspace), p.P, p.cols.data(), p.park(workspace),
                       static_cast<hipStream_t>(stream));
 }
 
@@ -226,14 +247,15 @@ int dpsgd_per_example_norms_multi_noalloc(const dpsgd_layer* layers, int32_t n_l
   if (st != DPSGD_OK) return st;
   if (!valid_mode(mode)) return DPSGD_ERR_UNSUPPORTED;
   if (!norms_sq) return DPSGD_ERR_INVALID_ARG;
-  const NormPlan p = plan_norms(layers, n_layers, mode);
+  // No park area: T > 256 Gram-form layers take the 128-row tiles here.
+  const NormPlan p = plan_norms(layers, n_layers, mode, false);
   if (p.bytes > DPSGD_NOALLOC_SCRATCH_BYTES) return DPSGD_ERR_WORKSPACE;
   void* ws = scratch_on_current_device(&st);
   if (!ws) return st;
   // Every partial slot [i][col] of the plan is written by exactly one job
   // before the reduction reads it, so the scratch needs no clearing.
   return launch_norms(layers, p.forms.data(), n_layers, norms_sq, accumulate ? 1 : 0,
-                      static_cast<float*>(ws), p.P, p.cols.data(),
+                      static_cast<float*>(ws), p.P, p.cols.data(), nullptr,
                       static_cast<hipStream_t>(stream));
 }
 
@@ -334,7 +356,7 @@ int dpsgd_clipped_sum_multi(const dpsgd_layer* layers, int32_t n_layers, int32_t
   // partials, then the per-example sums.
   if (!p.other.empty()) {
     st = launch_norm_partials(layers, p.norms.forms.data(), n_layers, partials, p.norms.P,
-                              p.norms.cols.data(), s);
+                              p.norms.cols.data(), p.norms.park(workspace), s);
     if (st != DPSGD_OK) return st;
   }
   if (n_st > 0) {

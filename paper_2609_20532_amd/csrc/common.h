@@ -16,7 +16,9 @@ constexpr int kMaxLayersPerLaunch = 48;  // entries of a per-launch layer table 
 // Norm form actually run for a layer (T = 1 always uses the closed form).
 // FORM_STORED (only in dpsgd_clipped_sum_multi): per-example gradients of a
 // layer with a narrow side are formed once, stored and normed (skinny.hip).
-enum NormForm : int { FORM_T1 = 0, FORM_GHOST = 1, FORM_MAT = 2, FORM_STORED = 3 };
+// FORM_GHOST256: the Gram form on 256-row tiles (T > 256, ghost.hip), chosen
+// by the workspace plans for FORM_GHOST layers that qualify.
+enum NormForm : int { FORM_T1 = 0, FORM_GHOST = 1, FORM_MAT = 2, FORM_STORED = 3, FORM_GHOST256 = 4 };
 constexpr int64_t kSkinnyMaxRank = 16;   // narrow side of a FORM_STORED layer
 
 // ----------------------------------------------------------- device helpers
@@ -71,13 +73,16 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form);
 NormForm resolve_norm_form(const dpsgd_layer& L, int32_t mode);
 
 // Writes per-example partials partials[i * P + col_l + j] for the given layers
-// (all with the chosen forms), then reduces them into norms_sq.
+// (all with the chosen forms), then reduces them into norms_sq. park: the
+// FORM_GHOST256 layers' park area (ghost256_park_bytes of their jobs), else
+// unused.
 int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
                  float* norms_sq, int accumulate, float* partials, int64_t P,
-                 const int64_t* cols, hipStream_t stream);
+                 const int64_t* cols, float* park, hipStream_t stream);
 // The two halves of launch_norms; the partials pass skips FORM_STORED layers.
 int launch_norm_partials(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
-                         float* partials, int64_t P, const int64_t* cols, hipStream_t stream);
+                         float* partials, int64_t P, const int64_t* cols, float* park,
+                         hipStream_t stream);
 int launch_norms_reduce(const float* partials, int64_t P, int64_t B, float* norms_sq,
                         int accumulate, hipStream_t stream);
 
@@ -109,6 +114,16 @@ int launch_gram64(const dpsgd_layer* layers, const int* idx, int n, const int64_
                   float* partials, int64_t P, hipStream_t stream);
 int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream);
+// Gram-form norms on 256-row tiles (ghost.hip): ghost_dma_ok layers with
+// T > 256, ghost256_pairs partials per example. At most kGhost256MaxGrid
+// workgroups run, each parking a 256 KB float32 tile in the park area
+// (ghost256_park_bytes for a call's total job count, B x pairs summed).
+constexpr int64_t kGhost256MaxGrid = 512;
+bool ghost256_ok(const dpsgd_layer& L);
+int64_t ghost256_pairs(const dpsgd_layer& L);
+size_t ghost256_park_bytes(int64_t jobs);
+int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                    float* partials, int64_t P, float* park, hipStream_t stream);
 
 bool tr_tile_ok(const dpsgd_layer& L);
 // k-major float32 kernel (gemm.hip): float32, T a multiple of 32, d_in and d_out

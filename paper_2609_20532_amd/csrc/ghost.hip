@@ -409,11 +409,304 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
   }
 }
 
+// ------------------------------------------------------- 256-row tiles
+//
+// For T > 256 a workgroup owns one 256 x 256 tile (p, q), p <= q, of the upper
+// triangle. Every row copied into LDS then takes part in 256 multiply-adds per
+// column instead of 128, so a tile moves half the bytes per FLOP of the
+// 128-row kernel above. The two float32 Gram tiles of a 256 x 256 tile
+// (512 KB) would fill the whole register file; instead GA is accumulated
+// first and each lane parks its accumulators in the workspace (written and
+// read back only by that lane), GG reuses the same registers, and the lanes
+// read GA back for the elementwise product. WAVES waves form a (WAVES / 2) x 2
+// grid of sub-tiles of kMB x 4 blocks of 32 x 32: 64 x 128 for eight waves,
+// 128 x 128 for four. The grid is capped at
+// kGhost256MaxGrid workgroups, each with a park slot of its own; workgroup b
+// takes jobs b, b + grid, ... .
+
+constexpr int kG4Rows = 256;
+constexpr int kG4ParkFloats = kG4Rows * kG4Rows;   // per workgroup
+constexpr int kG4BK = 64;                          // columns per slice
+constexpr int kG4Waves = 8;
+
+template <int BK, int WAVES>
+struct G4Cfg {
+  static constexpr int kThreads = 64 * WAVES;
+  static constexpr int kMB = 2 * 8 / WAVES;                 // 32-row blocks per wave along p
+  static constexpr int kNB = 4;                             // 32-row blocks per wave along q
+  static constexpr int kRowBytes = 2 * BK;                  // one row of a slice
+  static constexpr int kChunks = BK / 8;                    // 16-byte chunks per row
+  static constexpr int kRowsPerCopy = 1024 / kRowBytes;     // rows per copy instruction
+  static constexpr int kBlockBytes = kG4Rows * kRowBytes;   // one 256-row block of a slice
+  static constexpr int kStageBytes = 2 * kBlockBytes;       // blocks p and q
+  static constexpr int kStages = BK == 64 ? 2 : 4;
+  static constexpr int kLdsBytes = kStages * kStageBytes;   // 128 KB
+  static constexpr int kCopiesPerBlock = kG4Rows / kRowsPerCopy / WAVES;   // per wave
+  static constexpr int kSteps = BK / 16;                    // MFMA k steps per slice
+  static constexpr int kParkPerWave = kG4ParkFloats / WAVES;
+  // LDS slot of chunk c of row r is c ^ swz(r): the 16-lane operand reads
+  // (16 consecutive rows, one chunk) then touch 16 distinct 16-byte bank groups.
+  __host__ __device__ static constexpr int swz(int r) {
+    return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+  }
+};
+
+struct G4Args {
+  GhEntry L[kMaxLayersPerLaunch];
+  int32_t n;
+  uint32_t jobs;
+  int64_t P;
+  float* partials;
+  float* park;   // kG4ParkFloats per workgroup of the grid
+};
+
+// sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] of 256 x 256 tile (p, q) of example i.
+template <int BK, int WAVES, bool DIAG>
+__device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* lds, float* park) {
+  using C = G4Cfg<BK, WAVES>;
+  constexpr int MB = C::kMB, NB = C::kNB;
+  const int lane = threadIdx.x & 63;
+  const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = (int)(wave_u >> 1), wn = (int)(wave_u & 1u);
+  const int T = E.T;
+  const int rows_p = min(kG4Rows, T - kG4Rows * p);
+  const int rows_q = min(kG4Rows, T - kG4Rows * q);
+  const int nA = E.d_in / BK, n = nA + E.d_out / BK;
+  const char* Ab = static_cast<const char*>(E.A) + i * (int64_t)T * E.d_in * 2;
+  const char* Gb = static_cast<const char*>(E.G) + i * (int64_t)T * E.d_out * 2;
+  const uint32_t lds0 = lds_address(lds);
+
+  // Copy u of this wave fills the kRowsPerCopy rows starting at kRowsPerCopy j
+  // (j = wave + WAVES (u % kPer)) of block p (u < kPer) or block q: lane l
+  // takes row kRowsPerCopy j + l / kChunks and the global chunk that belongs
+  // in its slot l % kChunks. The slot swizzle of that row does not depend on
+  // u (kRowsPerCopy WAVES is a multiple of the swizzle period), so a lane's
+  // chunk is fixed; its row is clamped to the block's last valid row (rows
+  // past T repeat it, in bounds, and are masked out of the sum).
+  constexpr int kPer = C::kCopiesPerBlock;
+  constexpr int kCopies = DIAG ? kPer : 2 * kPer;
+  static_assert((C::kRowsPerCopy * WAVES) % 16 == 0, "both swizzles repeat every 16 rows");
+  const int r0 = C::kRowsPerCopy * (int)wave_u + lane / C::kChunks;   // row of copy u = 0
+  const uint32_t chunk16 = 16u * (uint32_t)((lane % C::kChunks) ^ C::swz(r0));
+  auto issue = [&](int s, int slot) {
+    const bool a = s < nA;
+    const char* src = a ? Ab + (int64_t)s * BK * 2 : Gb + (int64_t)(s - nA) * BK * 2;
+    const uint32_t stride = (uint32_t)(a ? E.d_in : E.d_out) * 2u;
+    const uint32_t dst = lds0 + (uint32_t)slot * C::kStageBytes;
+#pragma unroll
+    for (int u = 0; u < kCopies; ++u) {
+      const bool second = u >= kPer;
+      const int r = r0 + C::kRowsPerCopy * WAVES * (u % kPer);
+      const int row = kG4Rows * (second ? q : p) + min(r, (second ? rows_q : rows_p) - 1);
+      const uint32_t dst_off = (second ? (uint32_t)C::kBlockBytes : 0u) +
+                               1024u * ((uint32_t)wave_u + WAVES * (u % kPer));
+      copy16_to_lds(src, (uint32_t)row * stride + chunk16, dst + dst_off);
+    }
+  };
+
+  // Operand reads: lane l supplies row (l % 32) of a 32-row block and chunk
+  // 2 st + l / 32 of k step st.
+  const int g = lane >> 5;
+  uint32_t rd[C::kSteps];
+#pragma unroll
+  for (int st = 0; st < C::kSteps; ++st)
+    rd[st] = (uint32_t)((lane & 31) * C::kRowBytes + 16 * ((2 * st + g) ^ C::swz(lane & 31)));
+  const uint32_t rowA = (uint32_t)(32 * MB * wm * C::kRowBytes);
+  const uint32_t rowB = (DIAG ? 0u : (uint32_t)C::kBlockBytes) + (uint32_t)(32 * NB * wn * C::kRowBytes);
+
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[a][b] = f32x16_t{};
+
+  // All waves must be done with the ring (and the previous job's reduction
+  // slots) before this tile overwrites it.
+  __syncthreads();
+#pragma unroll
+  for (int d = 0; d < C::kStages - 1; ++d)
+    if (d < n) issue(d, d);
+
+  auto slice = [&](int s) {
+    // This wave's copies of slice s have landed once at most the later
+    // slices' copies are outstanding (at the first GG slice the park stores
+    // are outstanding too, so that wait is for everything); the barrier makes
+    // every wave's part visible and guarantees slice s - 1, whose slot is
+    // refilled next, is no longer read.
+    const int later = n - 1 - s;
+    if (s == nA) wait_vmcnt<0>();
+    else if (later >= C::kStages - 2) wait_vmcnt<kCopies * (C::kStages - 2)>();
+    else if (later == 1) wait_vmcnt<kCopies>();
+    else wait_vmcnt<0>();
+    barrier_no_wait();
+    if (s + C::kStages - 1 < n) issue(s + C::kStages - 1, (s + C::kStages - 1) % C::kStages);
+    typedef __attribute__((address_space(3))) const bf16x8_t lds_frag;
+    const char* base = lds + (s % C::kStages) * C::kStageBytes;
+    // Operands of k step st + 1 are read while the MFMAs of step st run; the
+    // scheduling barrier keeps the reads of later steps from being hoisted
+    // further (which would hold every step's operands in registers at once).
+    bf16x8_t fa[2][MB], fb[2][NB];
+    auto load = [&](int st, int buf) {
+#pragma unroll
+      for (int a = 0; a < MB; ++a) fa[buf][a] = *(lds_frag*)(base + rowA + 32 * a * C::kRowBytes + rd[st]);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) fb[buf][b] = *(lds_frag*)(base + rowB + 32 * b * C::kRowBytes + rd[st]);
+    };
+    load(0, 0);
+#pragma unroll
+    for (int st = 0; st < C::kSteps; ++st) {
+      if (st + 1 < C::kSteps) load(st + 1, (st + 1) & 1);
+#pragma unroll
+      for (int a = 0; a < MB; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[st & 1][a], fb[st & 1][b], acc[a][b], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // Park slot of this lane: float4 k (k = 4 (NB a + b) + c holds elements
+  // 4 c .. 4 c + 3 of block (a, b)) at float offset kParkPerWave wave + 256 k +
+  // 4 lane, so every store and load instruction covers 1 KB contiguously.
+  float* mine = park + C::kParkPerWave * (int)wave_u + 4 * lane;
+  for (int s = 0; s < nA; ++s) slice(s);
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        *reinterpret_cast<f32x4_t*>(mine + 256 * (4 * (NB * a + b) + c)) =
+            f32x4_t{acc[a][b][4 * c], acc[a][b][4 * c + 1], acc[a][b][4 * c + 2], acc[a][b][4 * c + 3]};
+      acc[a][b] = f32x16_t{};
+      __builtin_amdgcn_sched_barrier(0);   // one block's values in flight at a time
+    }
+  for (int s = nA; s < n; ++s) slice(s);
+
+  // Element v of block (a, b) in lane l: tile row 32 (MB wm + a) + 8 (v / 4) +
+  // 4 (l / 32) + v % 4, column 32 (NB wn + b) + l % 32. A diagonal tile is
+  // computed whole, so its sum is the plain sum over the tile as well.
+  float sum = 0.f;
+#pragma unroll
+  for (int a = 0; a < MB; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      f32x4_t ga[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        ga[c] = *reinterpret_cast<const f32x4_t*>(mine + 256 * (4 * (NB * a + b) + c));
+      const int col = 32 * (NB * wn + b) + (lane & 31);
+      float blk = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = 32 * (MB * wm + a) + 8 * (v >> 2) + 4 * g + (v & 3);
+        const float x = ga[v >> 2][v & 3] * acc[a][b][v];
+        blk += (row < rows_p && col < rows_q) ? x : 0.f;
+      }
+      sum += blk;
+      __builtin_amdgcn_sched_barrier(0);   // one block's parked values in flight at a time
+    }
+  return sum;
+}
+
+template <int BK, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void ghost_tile256_kernel(G4Args args) {
+  __shared__ __attribute__((aligned(1024))) char lds[G4Cfg<BK, WAVES>::kLdsBytes];
+  float* park = args.park + (size_t)blockIdx.x * kG4ParkFloats;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // Consecutive logical indices (the tiles of one example) run on one XCD, so
+  // the rows that two tiles share are fetched from HBM into that XCD's L2 once.
+  for (uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x); job < args.jobs; job += gridDim.x) {
+    int l = 0;
+    {
+      int lo = 0, hi = args.n - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (args.L[mid].wg_begin <= job) lo = mid; else hi = mid - 1;
+      }
+      l = lo;
+    }
+    const GhEntry& E = args.L[l];
+    const uint32_t w = job - E.wg_begin;
+    const int64_t i = w / (uint32_t)E.pairs;
+    int pr = (int)(w % (uint32_t)E.pairs);
+    const int pr0 = pr;
+    int p = 0;
+    while (pr >= E.nt - p) {
+      pr -= E.nt - p;
+      ++p;
+    }
+    const int q = p + pr;
+    float s = p == q ? ghost_tile256<BK, WAVES, true>(E, i, p, q, lds, park)
+                     : 2.0f * ghost_tile256<BK, WAVES, false>(E, i, p, q, lds, park);
+    s = wave_sum(s);
+    __syncthreads();   // the ring is free again
+    float* red = reinterpret_cast<float*>(lds);
+    if (lane == 0) red[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float v = 0.f;
+#pragma unroll
+      for (int k = 0; k < WAVES; k += 2) v += red[k] + red[k + 1];
+      args.partials[i * args.P + E.partial_col + pr0] = v;
+    }
+  }
+}
+
 }  // namespace
 
 bool ghost_dma_ok(const dpsgd_layer& L) {
   return L.dtype == DPSGD_BF16 && L.d_in % kGgBK == 0 && L.d_out % kGgBK == 0 &&
          L.T * L.d_in * 2 < (INT64_C(1) << 31) && L.T * L.d_out * 2 < (INT64_C(1) << 31);
+}
+
+bool ghost256_ok(const dpsgd_layer& L) { return L.T > kG4Rows && ghost_dma_ok(L); }
+
+int64_t ghost256_pairs(const dpsgd_layer& L) {
+  const int64_t nt = ceil_div(L.T, kG4Rows);
+  return nt * (nt + 1) / 2;
+}
+
+size_t ghost256_park_bytes(int64_t jobs) {
+  const int64_t grid = jobs < kGhost256MaxGrid ? jobs : kGhost256MaxGrid;
+  return (size_t)grid * kG4ParkFloats * sizeof(float);
+}
+
+int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
+                    float* partials, int64_t P, float* park, hipStream_t stream) {
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    G4Args a{};
+    a.n = m;
+    a.P = P;
+    a.partials = partials;
+    a.park = park;
+    int64_t jobs = 0;
+    for (int k = 0; k < m; ++k) {
+      const dpsgd_layer& L = layers[idx[base + k]];
+      GhEntry E{};
+      E.A = L.A;
+      E.G = L.G;
+      E.d_in = (int32_t)L.d_in;
+      E.d_out = (int32_t)L.d_out;
+      E.T = (int32_t)L.T;
+      E.nt = (int32_t)ceil_div(L.T, kG4Rows);
+      E.pairs = E.nt * (E.nt + 1) / 2;
+      E.partial_col = (int32_t)cols[idx[base + k]];
+      E.wg_begin = (uint32_t)jobs;
+      a.L[k] = E;
+      jobs += L.B * (int64_t)E.pairs;
+    }
+    if (jobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
+    a.jobs = (uint32_t)jobs;
+    // The launches of one call run in stream order, so they share the park
+    // area (sized for the largest grid).
+    const int64_t grid = jobs < kGhost256MaxGrid ? jobs : kGhost256MaxGrid;
+    hipLaunchKernelGGL((ghost_tile256_kernel<kG4BK, kG4Waves>), dim3((uint32_t)grid),
+                       dim3(64 * kG4Waves), 0, stream, a);
+    if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+  }
+  return DPSGD_OK;
 }
 
 int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,

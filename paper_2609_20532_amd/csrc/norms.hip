@@ -299,22 +299,25 @@ bool ghost_vec_ok(const dpsgd_layer& L) {
 
 template <typename TIn>
 int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
-                       float* partials, int64_t P, const int64_t* cols, hipStream_t stream) {
+                       float* partials, int64_t P, const int64_t* cols, float* park,
+                       hipStream_t stream) {
   const int64_t B = layers[0].B;
   int idx_t1[256], n_t1 = 0;
   int idx_gv[256], n_gv = 0;
   int idx_gs[256], n_gs = 0;
   int idx_gd[256], n_gd = 0;
+  int idx_g4[256], n_g4 = 0;
   int idx_g64[256], n_g64 = 0;
   int idx_mat[256], n_mat = 0;
   for (int base = 0; base < n_layers; base += 256) {
-    n_t1 = n_gv = n_gs = n_gd = n_g64 = n_mat = 0;
+    n_t1 = n_gv = n_gs = n_gd = n_g4 = n_g64 = n_mat = 0;
     const int m = n_layers - base < 256 ? n_layers - base : 256;
     for (int k = 0; k < m; ++k) {
       const int l = base + k;
       switch (forms[l]) {
         case FORM_T1: idx_t1[n_t1++] = l; break;
         case FORM_STORED: break;   // skinny.hip
+        case FORM_GHOST256: idx_g4[n_g4++] = l; break;
         case FORM_GHOST:
           if (ghost_dma_ok(layers[l])) idx_gd[n_gd++] = l;
           else if (gram64_ok(layers[l])) idx_g64[n_g64++] = l;
@@ -331,6 +334,8 @@ int launch_norms_typed(const dpsgd_layer* layers, const NormForm* forms, int n_l
     if (st == DPSGD_OK && n_gs)
       st = launch_ghost_group<TIn, false>(layers, idx_gs, n_gs, cols, partials, P, stream);
     if (st == DPSGD_OK && n_gd) st = launch_ghost_dma(layers, idx_gd, n_gd, cols, partials, P, stream);
+    if (st == DPSGD_OK && n_g4)
+      st = launch_ghost256(layers, idx_g4, n_g4, cols, partials, P, park, stream);
     if (st == DPSGD_OK && n_g64) st = launch_gram64(layers, idx_g64, n_g64, cols, partials, P, stream);
     if (st == DPSGD_OK && n_mat)
       st = launch_mat_norms(layers, idx_mat, n_mat, cols, partials, P, stream);
@@ -363,6 +368,7 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
   switch (form) {
     case FORM_T1: return 1;
     case FORM_STORED: return skinny_chunks(L);
+    case FORM_GHOST256: return ghost256_pairs(L);
     case FORM_GHOST: {
       const int64_t nt = ceil_div(L.T, kTile);
       return nt * (nt + 1) / 2;
@@ -373,10 +379,11 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
 }
 
 int launch_norm_partials(const dpsgd_layer* layers, const NormForm* forms, int n_layers,
-                         float* partials, int64_t P, const int64_t* cols, hipStream_t stream) {
+                         float* partials, int64_t P, const int64_t* cols, float* park,
+                         hipStream_t stream) {
   return layers[0].dtype == DPSGD_BF16
-             ? launch_norms_typed<uint16_t>(layers, forms, n_layers, partials, P, cols, stream)
-             : launch_norms_typed<float>(layers, forms, n_layers, partials, P, cols, stream);
+             ? launch_norms_typed<uint16_t>(layers, forms, n_layers, partials, P, cols, park, stream)
+             : launch_norms_typed<float>(layers, forms, n_layers, partials, P, cols, park, stream);
 }
 
 int launch_norms_reduce(const float* partials, int64_t P, int64_t B, float* norms_sq,
@@ -388,9 +395,9 @@ int launch_norms_reduce(const float* partials, int64_t P, int64_t B, float* norm
 }
 
 int launch_norms(const dpsgd_layer* layers, const NormForm* forms, int n_layers, float* norms_sq,
-                 int accumulate, float* partials, int64_t P, const int64_t* cols,
+                 int accumulate, float* partials, int64_t P, const int64_t* cols, float* park,
                  hipStream_t stream) {
-  const int st = launch_norm_partials(layers, forms, n_layers, partials, P, cols, stream);
+  const int st = launch_norm_partials(layers, forms, n_layers, partials, P, cols, park, stream);
   if (st != DPSGD_OK) return st;
   return launch_norms_reduce(partials, P, layers[0].B, norms_sq, accumulate, stream);
 }

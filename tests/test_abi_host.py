@@ -50,9 +50,16 @@ def test_workspace_queries_and_mode_selection(lib):
     assert dpsgd.dpsgd_select_norm_mode(c3) == dpsgd.DPSGD_NORM_GHOST
     lora = dpsgd.shape_layer(16, 1024, 4096, 16)
     assert dpsgd.dpsgd_select_norm_mode(lora) == dpsgd.DPSGD_NORM_MATERIALIZE
-    # 4 T-tiles -> 10 upper-triangle tile pairs per example
-    assert dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 64 * 10 * 4 + 0 \
-        or dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 2560
+    # T = 512 bf16 runs the Gram form on 256-row tiles: 3 upper-triangle tile
+    # pairs per example (partials 64 x 3 floats, rounded to 256 bytes), then a
+    # 256 KB float32 park slot per workgroup of the 192-job grid.
+    assert dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 768 + 192 * 262144
+    # More than 512 jobs: the grid (and the park area) stays at 512 workgroups.
+    big = dpsgd.shape_layer(200, 520, 64, 64)    # 3 row blocks, 6 pairs, 1200 jobs
+    assert dpsgd.dpsgd_norms_workspace_bytes(big, dpsgd.DPSGD_NORM_GHOST) == 4864 + 512 * 262144
+    # float32 keeps the 128-row tiles (4 T-tiles -> 10 pairs) and no park area.
+    c3f = dpsgd.shape_layer(64, 512, 768, 3072, dpsgd.DPSGD_F32)
+    assert dpsgd.dpsgd_norms_workspace_bytes(c3f, dpsgd.DPSGD_NORM_GHOST) == 2560
     t1 = dpsgd.shape_layer(32, 1, 256, 128, dpsgd.DPSGD_F32)
     assert dpsgd.dpsgd_norms_workspace_bytes(t1) == 256   # one partial per example, rounded
     assert dpsgd.dpsgd_clip_workspace_bytes(t1) > 0

@@ -299,3 +299,169 @@ def test_skinny_mfma_lanes_form_the_gradient(T, d_w, r, narrow_is_a, chunk, t0, 
     np.testing.assert_allclose(got[sl], ref[sl], rtol=1e-12, atol=1e-12)
     # The wave's norm partial (every output, zeros included) is the chunk's.
     assert math.isclose(float(np.sum(acc ** 2)), float(np.sum(ref[sl] ** 2)), rel_tol=1e-12)
+
+
+# ------------------------- bf16 Gram form on 256-row tiles (ghost_tile256_kernel)
+#
+# WAVES waves own a 256 x 256 tile (p, q): a (WAVES / 2) x 2 grid of sub-tiles
+# of MB x 4 blocks of 32 x 32 (MB = 16 / WAVES). Slices of BK columns of row
+# blocks p and q are copied into LDS (1 KB per copy instruction) and read back
+# as the 32x32x16 MFMA operands; GA is parked per lane in the workspace; a
+# diagonal tile is computed whole.
+
+G4_ROWS = 256
+
+
+def g4_swz(bk, r):
+    return ((r >> 1) & 7) if bk == 64 else ((r >> 2) & 3)
+
+
+def xcd_logical_index(bid, nwg):
+    per, rem, xcd, idx = nwg >> 3, nwg & 7, bid & 7, bid >> 3
+    return xcd * (per + 1) + idx if xcd < rem else rem * (per + 1) + (xcd - rem) * per + idx
+
+
+def g4_stage(bk, waves, T, d, p, q, s):
+    """LDS stage of slice s of a d-wide operand: {16-byte slot: (row, chunk)}."""
+    row_bytes, chunks = 2 * bk, bk // 8
+    rpc = 1024 // row_bytes
+    per = G4_ROWS // rpc // waves
+    diag = p == q
+    rows_p, rows_q = min(256, T - 256 * p), min(256, T - 256 * q)
+    lds = {}
+    for wave in range(waves):
+        r0 = rpc * wave + np.arange(64) // chunks              # row of copy u = 0 per lane
+        chunk = (np.arange(64) % chunks) ^ np.array([g4_swz(bk, r) for r in r0])
+        for u in range(per if diag else 2 * per):
+            second = u >= per
+            j = wave + waves * (u % per)
+            for lane in range(64):
+                r = rpc * j + lane // chunks
+                assert r == r0[lane] + rpc * waves * (u % per)
+                assert g4_swz(bk, r) == g4_swz(bk, int(r0[lane])), "swizzle depends on u"
+                rv = rows_q if second else rows_p
+                row = 256 * (q if second else p) + min(r, rv - 1)
+                off = row * d * 2 + 16 * int(chunk[lane]) + s * bk * 2
+                assert 0 <= off and off + 16 <= T * d * 2 and off % 16 == 0
+                dst = (G4_ROWS * row_bytes if second else 0) + 1024 * j + 16 * lane
+                assert dst + 16 <= 2 * G4_ROWS * row_bytes
+                assert dst not in lds, "an LDS slot written twice"
+                lds[dst] = (row, s * chunks + int(chunk[lane]))
+    expect = (1 if diag else 2) * G4_ROWS * row_bytes // 16
+    assert len(lds) == expect, "an LDS slot left unwritten"
+    return lds
+
+
+def g4_gram(bk, waves, X, T, p, q):
+    """GA (or GG) of tile (p, q) as the waves' accumulators: {(wave, a, b): 32x32}."""
+    d = X.shape[1]
+    row_bytes = 2 * bk
+    mb, nb = 16 // waves, 4
+    diag = p == q
+    acc = {}
+    for s in range(d // bk):
+        lds = g4_stage(bk, waves, T, d, p, q, s)
+        for wave in range(waves):
+            wm, wn = wave >> 1, wave & 1
+            row_a = 32 * mb * wm * row_bytes
+            row_b = (0 if diag else G4_ROWS * row_bytes) + 32 * nb * wn * row_bytes
+            for st in range(bk // 16):
+                frag = {}
+                for which, base, nblk in (("a", row_a, mb), ("b", row_b, nb)):
+                    for blk in range(nblk):
+                        rows, ks, addrs = [], [], []
+                        for lane in range(64):
+                            g = lane >> 5
+                            rd = (lane & 31) * row_bytes + 16 * ((2 * st + g) ^ g4_swz(bk, lane & 31))
+                            addr = base + 32 * blk * row_bytes + rd
+                            addrs.append(addr)
+                            row, chunk = lds[addr]
+                            rows.append(row)
+                            ks.append(chunk)
+                        # 16-lane groups read 16 distinct 16-byte bank groups (256 B of banks).
+                        for g16 in range(4):
+                            grp = {(a // 16) % 16 for a in addrs[16 * g16:16 * g16 + 16]}
+                            assert len(grp) == 16, "LDS bank conflict in an operand read"
+                        # lane l: row (l % 32) of the 32-row block, k chunk 2 st + l / 32
+                        assert all(rows[i] == rows[i + 32] and ks[i + 32] == ks[i] + 1 for i in range(32))
+                        frag[(which, blk)] = (rows, ks)
+                for a in range(mb):
+                    for b in range(nb):
+                        ra, ka = frag[("a", a)]
+                        rb, kb = frag[("b", b)]
+                        A32 = np.stack([X[ra[i], 8 * ka[i]:8 * ka[i] + 16] for i in range(32)])
+                        B32 = np.stack([X[rb[i], 8 * kb[i]:8 * kb[i] + 16] for i in range(32)])
+                        key = (wave, a, b)
+                        acc[key] = acc.get(key, np.zeros((32, 32))) + A32 @ B32.T
+    return acc
+
+
+def g4_tile_sum(bk, waves, A, G, T, p, q):
+    GA = g4_gram(bk, waves, A, T, p, q)
+    GG = g4_gram(bk, waves, G, T, p, q)
+    mb, nb = 16 // waves, 4
+    per_wave = 256 * 256 // waves
+    rows_p, rows_q = min(256, T - 256 * p), min(256, T - 256 * q)
+    park = np.full(256 * 256, np.nan)
+    lane = np.arange(64)
+    v = np.arange(16)
+    # Lane l, element v: block row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
+    br = 8 * (v[None, :] >> 2) + 4 * (lane[:, None] >> 5) + (v[None, :] & 3)
+    bc = np.broadcast_to(lane[:, None] & 31, br.shape)
+    total = 0.0
+    for wave in range(waves):
+        wm, wn = wave >> 1, wave & 1
+        for a in range(mb):
+            for b in range(nb):
+                lane_ga = GA[(wave, a, b)][br, bc]
+                # Park: float4 k = 4 (NB a + b) + c holds elements 4c..4c+3.
+                offs = [per_wave * wave + 256 * (4 * (nb * a + b) + c) + 4 * lane[:, None]
+                        + np.arange(4)[None, :] for c in range(4)]
+                for c in range(4):
+                    assert np.all(offs[c] < 256 * 256)
+                    assert np.all(np.isnan(park[offs[c]])), "park slot written twice"
+                    park[offs[c]] = lane_ga[:, 4 * c:4 * c + 4]
+                back = np.concatenate([park[o] for o in offs], axis=1)
+                row = 32 * (mb * wm + a) + br
+                col = 32 * (nb * wn + b) + bc
+                mask = (row < rows_p) & (col < rows_q)
+                total += float(np.sum(np.where(mask, back * GG[(wave, a, b)][br, bc], 0.0)))
+    assert not np.any(np.isnan(park)), "park slot never written"
+    return total
+
+
+@pytest.mark.parametrize("bk,waves", [(64, 8), (64, 4), (32, 8)])
+@pytest.mark.parametrize("T,d_in,d_out", [(300, 64, 128), (257, 128, 64), (520, 64, 64),
+                                          (512, 64, 64)])
+def test_ghost256_tiles_give_the_norm(bk, waves, T, d_in, d_out):
+    rng = np.random.default_rng(T + d_in + bk + waves)
+    A = rng.integers(-3, 4, (T, d_in)).astype(np.float64)
+    G = rng.integers(-3, 4, (T, d_out)).astype(np.float64)
+    nt = -(-T // 256)
+    total = 0.0
+    seen = set()
+    for pr0 in range(nt * (nt + 1) // 2):
+        pr, p = pr0, 0
+        while pr >= nt - p:
+            pr -= nt - p
+            p += 1
+        q = p + pr
+        assert p <= q < nt and (p, q) not in seen
+        seen.add((p, q))
+        t = g4_tile_sum(bk, waves, A, G, T, p, q)
+        total += t if p == q else 2.0 * t
+    assert len(seen) == nt * (nt + 1) // 2
+    want = float(np.sum((G.T @ A) ** 2))
+    assert total == pytest.approx(want, rel=1e-12)
+
+
+@pytest.mark.parametrize("jobs", [1, 7, 160, 192, 511, 512, 513, 1080, 4099])
+def test_ghost256_grid_visits_every_job_once(jobs):
+    grid = min(jobs, 512)
+    visits = []
+    for bid in range(grid):
+        job = xcd_logical_index(bid, grid)
+        while job < jobs:
+            visits.append(job)
+            job += grid
+    assert sorted(visits) == list(range(jobs))
