@@ -44,11 +44,22 @@ GEMM_SOURCES = [os.path.join(HERE, "paper_2609_20532_amd", "csrc", f)
 
 
 def dominant_kernel(W) -> str:
-    """The clip kernel that carries the workload's bf16 layers: the 384x256-tile
-    kernel when every layer fits it, else the 256x256-tile kernel."""
-    wide = all(W.dtype == "bf16" and s.d_out % 384 == 0 and s.d_in % 256 == 0 and W.T % 32 == 0
-               for s in W.layers)
-    return "tgemm_wide_kernel" if wide else "tgemm_tr_kernel<0>"
+    """The clip kernel that carries the workload's largest layer (the library's
+    rules): bf16 on the 384x256-tile kernel when d_in % 256 == 0, T % 64 == 0 and
+    d_out % 384 == 0, or d_out % 32 == 0 with a ragged last row tile padding at
+    most 6 % on a layer of at least one tile per CU; else bf16 on the 256x256-tile
+    kernel when both widths are multiples of 256; else the 128-tile kernel."""
+    s = max(W.layers, key=lambda s: s.d_in * s.d_out)
+    if W.dtype != "bf16":
+        return "tgemm_kernel"
+    tiles_m = -(-s.d_out // 384)
+    pad = tiles_m * 384 - s.d_out
+    ragged = s.d_out % 32 == 0 and 50 * pad <= 3 * s.d_out and tiles_m * (s.d_in // 256) >= 256
+    if s.d_in % 256 == 0 and W.T % 64 == 0 and (s.d_out % 384 == 0 or ragged):
+        return "tgemm_wide_kernel"
+    if s.d_in % 256 == 0 and s.d_out % 256 == 0 and W.T % 32 == 0:
+        return "tgemm_tr_kernel<0>"
+    return "tgemm_kernel"
 
 
 def parse():

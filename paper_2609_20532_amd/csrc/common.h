@@ -176,8 +176,10 @@ void plan_tr_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrC
 int launch_tr_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,
                    float* const* outs, int accumulate, const TrClipPlan& plan, float* tail_ws,
                    hipStream_t stream);
-// 384x256-tile clip kernel (gemm_wide.hip): bf16, d_out % 384 == 0,
-// d_in % 256 == 0, T % 32 == 0; preferred over the 256-tile kernel.
+// 384x256-tile clip kernel (gemm_wide.hip): bf16, d_in % 256 == 0, T % 64 == 0,
+// d_out % 384 == 0, or d_out % 32 == 0 with a ragged last row tile padding at
+// most 6 % of d_out when the layer has at least one round of tiles (one per
+// CU); preferred over the 256-tile kernel.
 bool wide_tile_ok(const dpsgd_layer& L);
 void plan_wide_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan);
 int launch_wide_clip(const dpsgd_layer* layers, const int* idx, int n, const float* factors,

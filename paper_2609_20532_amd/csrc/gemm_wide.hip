@@ -1,5 +1,7 @@
 // 384x256-tile transposed-operand MFMA GEMM for the clip-weighted sum of bf16
-// layers with d_out % 384 == 0 and d_in % 256 == 0:
+// layers with d_in % 256 == 0 and d_out a multiple of 32 (the last row tile
+// may hold fewer than 384 rows: its G copies repeat the last valid 64-byte
+// column block, and the rows past d_out are not stored):
 //   out[m][n] = sum_k c(k) G[k][m] A[k][n],  k over the B*T rows, c = c_i of
 //   the example i = k / T (paper: Section 2.2, the clipped per-example
 //   gradients c_i g_i summed over the batch).
@@ -133,6 +135,8 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
                             const float* factors, char* lds, WdAcc& acc) {
   const int M = E.M, N = E.N, T = E.T;
   const int spe = T / kWdBK;
+  // 32-column blocks of G inside the matrix (12 except in a ragged last row tile).
+  const uint32_t nvb = (uint32_t)min(kWdTM / 32, (M - tm * kWdTM) / 32);
   const int lane = threadIdx.x & 63;
   const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const char* Gt = static_cast<const char*>(E.G) + (int64_t)tm * kWdTM * 2;
@@ -153,7 +157,7 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
     const uint32_t t = wave_u + (uint32_t)(kWdWaves * p);
     if (p < kWdGCopies / kWdWaves) {
       const uint32_t row = 4u * (t / 3u) + l_row, blk = 4u * (t % 3u) + l_unit;
-      voff[p] = row * (uint32_t)M * 2u + 64u * blk + l_byte;
+      voff[p] = row * (uint32_t)M * 2u + 64u * min(blk, nvb - 1u) + l_byte;
     } else {
       const uint32_t u = t - (uint32_t)kWdGCopies;
       const uint32_t row = 4u * (u / 2u) + l_row, blk = 4u * (u % 2u) + l_unit;
@@ -265,16 +269,18 @@ __device__ float wd_segment(const WdEntry& E, int tm, int tn, int64_t q0, int64_
 }
 
 // Writes scale * acc into a 384 x 256 row-major destination (row stride ld),
-// adding what is there when add. Register v of block (i, j) in lane l is tile
-// row 32 (kWdMB wm + i) + 8 (v / 4) + 4 (l / 32) + v % 4, column 32 (kWdNB wn + j) + l % 32.
+// adding what is there when add; only the first nvb 32-row blocks (the rows
+// inside the matrix). Register v of block (i, j) in lane l is tile row
+// 32 (kWdMB wm + i) + 8 (v / 4) + 4 (l / 32) + v % 4, column 32 (kWdNB wn + j) + l % 32.
 __device__ __forceinline__ void wd_store(float* dst, int64_t ld, const WdAcc& acc, float scale,
-                                         bool add) {
+                                         bool add, int nvb) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / kWdWavesN, wn = wave % kWdWavesN;
   float* p0 = dst + (int64_t)(wm * kWdMB * 32 + 4 * (lane >> 5)) * ld + wn * kWdNB * 32 +
               (lane & 31);
 #pragma unroll
-  for (int i = 0; i < kWdMB; ++i)
+  for (int i = 0; i < kWdMB; ++i) {
+    if (wm * kWdMB + i >= nvb) break;   // wave-uniform
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       float* p = p0 + (int64_t)(32 * i + 8 * (v >> 2) + (v & 3)) * ld;
@@ -284,6 +290,7 @@ __device__ __forceinline__ void wd_store(float* dst, int64_t ld, const WdAcc& ac
         p[32 * j] = add ? p[32 * j] + x : x;
       }
     }
+  }
 }
 
 __device__ __forceinline__ uint32_t wd_range_begin(uint32_t k, uint32_t Q, uint32_t w) {
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(kWdThreads, 1) void tgemm_wide_kernel(WdArgs args) 
   float* dst = whole ? E.out + (int64_t)tm * kWdTM * E.N + tn * kWdTN
                      : args.partials + (int64_t)(job - args.n_full) * kWdTileElems;
   const int64_t ld = whole ? (int64_t)E.N : (int64_t)kWdTN;
-  wd_store(dst, ld, acc, c, whole && args.accumulate);
+  wd_store(dst, ld, acc, c, whole && args.accumulate, min(kWdTM / 32, (E.M - tm * kWdTM) / 32));
 }
 
 // Adds the tail_w partials of every tail tile in range order (deterministic)
@@ -344,6 +351,7 @@ __global__ __launch_bounds__(256) void wide_fixup_kernel(WdArgs args) {
   const int tm = tile / E.tiles_n, tn = tile % E.tiles_n;
   const int e = (int)(blockIdx.x % kChunks) * 1024 + threadIdx.x * 4;
   const int r = e / kWdTN, c = e % kWdTN;
+  if (tm * kWdTM + r >= E.M) return;   // rows past d_out of a ragged last row tile
   const float* src = args.partials + (int64_t)t_local * args.tail_w * kWdTileElems + e;
   float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k = 0; k < args.tail_w; ++k) {
@@ -360,10 +368,22 @@ __global__ __launch_bounds__(256) void wide_fixup_kernel(WdArgs args) {
 
 }  // namespace
 
+// Row tiles of a layer (the last one may be ragged).
+int64_t wide_tiles_m(const dpsgd_layer& L) { return ceil_div(L.d_out, kWdTM); }
+
 bool wide_tile_ok(const dpsgd_layer& L) {
   // Per-lane copy offsets are 32-bit: 32 k-rows of d * 2 bytes stay below 2^32.
-  return L.dtype == DPSGD_BF16 && L.d_out % kWdTM == 0 && L.d_in % kWdTN == 0 &&
-         L.T % kWdBK == 0 && L.d_in <= (INT64_C(1) << 24) && L.d_out <= (INT64_C(1) << 24);
+  // A ragged last row tile is taken when it pads at most 6 % of d_out and the
+  // layer has at least one round of tiles: with fewer, every tile would be
+  // split along K, and the 256 x 256 kernel, whose tiles fill the round, was
+  // faster (4096 x 4096, B T = 16384: 0.53 against 0.66 ms), while with
+  // several rounds the 384-row tile wins (11008 x 4096: 1.30 against 1.35 ms).
+  const int64_t tm = wide_tiles_m(L), pad = tm * kWdTM - L.d_out;
+  const bool whole = L.d_out % kWdTM == 0;
+  const bool ragged = L.d_out % 32 == 0 && 50 * pad <= 3 * L.d_out &&
+                      tm * (L.d_in / kWdTN) >= tr_cu_count();
+  return L.dtype == DPSGD_BF16 && (whole || ragged) && L.d_in % kWdTN == 0 && L.T % kWdBK == 0 &&
+         L.d_in <= (INT64_C(1) << 24) && L.d_out <= (INT64_C(1) << 24);
 }
 
 void plan_wide_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, TrClipPlan* plan) {
@@ -371,7 +391,7 @@ void plan_wide_clip(const dpsgd_layer* layers, const int* idx, int n, int cus, T
   bool uniform = true;
   for (int k = 0; k < n; ++k) {
     const dpsgd_layer& L = layers[idx[k]];
-    tiles += (L.d_out / kWdTM) * (L.d_in / kWdTN);
+    tiles += wide_tiles_m(L) * (L.d_in / kWdTN);
     const int64_t q = L.B * (L.T / kWdBK);
     if (Q >= 0 && q != Q) uniform = false;
     Q = q;
@@ -421,7 +441,7 @@ int launch_wide_clip(const dpsgd_layer* layers, const int* idx, int n, const flo
     E.tiles_n = (int32_t)(L.d_in / kWdTN);
     E.tile_begin = (uint32_t)tb;
     E.q_total = L.B * (L.T / kWdBK);
-    tb += (L.d_out / kWdTM) * E.tiles_n;
+    tb += wide_tiles_m(L) * E.tiles_n;
   }
   const int64_t jobs = plan.n_full + plan.n_tail;
   if (jobs <= 0) return DPSGD_OK;

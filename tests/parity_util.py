@@ -112,8 +112,23 @@ def weights_in_fp32(T: int, d_in: int, d_out: int, dtype: str, fused: bool = Fal
         return True
     if d_in * d_out <= 512:
         return True
-    big = d_in % 256 == 0 and (d_out % 256 == 0 or d_out % 384 == 0) and T % 32 == 0
-    return big or (T >= 64 and (-T) % 64 * 8 <= T)
+    return wide_tile(T, d_in, d_out) or tile256(T, d_in, d_out) or (T >= 64 and (-T) % 64 * 8 <= T)
+
+
+def wide_tile(T: int, d_in: int, d_out: int, cus: int = 256) -> bool:
+    """The library's rule for the 384x256-tile clip kernel (bf16): d_in a
+    multiple of 256, T of 64, and d_out of 384, or of 32 with the ragged last
+    row tile padding at most 6 % of d_out on a layer of at least one tile per
+    CU."""
+    tiles_m = -(-d_out // 384)
+    pad = tiles_m * 384 - d_out
+    ragged = d_out % 32 == 0 and 50 * pad <= 3 * d_out and tiles_m * (d_in // 256) >= cus
+    return d_in % 256 == 0 and T % 64 == 0 and (d_out % 384 == 0 or ragged)
+
+
+def tile256(T: int, d_in: int, d_out: int) -> bool:
+    """The library's rule for the 256x256-tile clip kernel (bf16)."""
+    return d_in % 256 == 0 and d_out % 256 == 0 and T % 32 == 0
 
 
 def sum_bound(T: int, d_in: int, d_out: int, dtype: str, fused: bool = False) -> float:

@@ -18,7 +18,8 @@ from oracle import philox
 from paper_2609_20532_amd import workloads as wl
 
 from parity_util import (TOL, assert_sum_close, check_step_outputs, device_layers, guard_band,
-                         oracle_layers, rel_err, run_step_keep_sums, sum_bound, torch_to_float64)
+                         oracle_layers, rel_err, run_step_keep_sums, sum_bound, torch_to_float64,
+                         weights_in_fp32)
 
 pytestmark = pytest.mark.gpu
 
@@ -230,20 +231,20 @@ CLIP_SHAPES = [
     (4, 64, 256, 384, wl.BF16),     # 384x256-tile kernel, one tile split along K
     (3, 128, 512, 768, wl.BF16),    # 384x256-tile kernel, four tiles, 2 slices per example
     (8, 256, 256, 384, wl.BF16),    # 384x256-tile kernel, d_out not a multiple of 256, long K
+    (1, 128, 6144, 4064, wl.BF16),  # 384x256-tile kernel, ragged last row tiles (224 of 384 rows), 264 tiles, split tail
+    (2, 64, 6144, 4064, wl.BF16),   # the same, one K slice per example
 ]
-TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-5:]
-K32_NARROW, K32_SQUARE = CLIP_SHAPES[-7:-5]
-TINY_JOBS, TINY_ONE_JOB = CLIP_SHAPES[-10:-8]
+TILE256_ONE_SPLIT, TILE256_SPLIT_K, WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_LONG_K = CLIP_SHAPES[-7:-2]
+WIDE_RAGGED_B1, WIDE_RAGGED_B2 = CLIP_SHAPES[-2:]
+K32_NARROW, K32_SQUARE = CLIP_SHAPES[-9:-7]
+TINY_JOBS, TINY_ONE_JOB = CLIP_SHAPES[-12:-10]
 TINY_BF16 = CLIP_SHAPES[5]
 
 
 def _weights_in_fp32(shape):
     """True when the clip weight is applied in fp32 (no bf16 rounding of c_i * G)."""
     B, T, d_in, d_out, dtype = shape
-    if dtype == wl.F32:
-        return True
-    big = d_in % 256 == 0 and (d_out % 256 == 0 or d_out % 384 == 0) and T % 32 == 0
-    return big or (T >= 64 and (-T) % 64 * 8 <= T)
+    return weights_in_fp32(T, d_in, d_out, dtype)
 
 
 def _clip_case(dp, shape, C, accumulate=False):
@@ -285,8 +286,8 @@ def test_clip_sum_matches_oracle(dp, shape):
 
 
 @pytest.mark.parametrize("shape", [CLIP_SHAPES[2], TILE256_ONE_SPLIT, TILE256_SPLIT_K,
-                                   WIDE_ONE_TILE, WIDE_FOUR_TILES, K32_NARROW, K32_SQUARE, TINY_JOBS,
-                                   TINY_BF16])
+                                   WIDE_ONE_TILE, WIDE_FOUR_TILES, WIDE_RAGGED_B2, K32_NARROW,
+                                   K32_SQUARE, TINY_JOBS, TINY_BF16])
 def test_zero_factor_examples_contribute_nothing(dp, shape):
     """An example whose squared norm is +inf gets factor C/inf = 0; with finite
     inputs its clipped gradient 0 * g_i is exactly zero (Section 2.2)."""

@@ -465,3 +465,53 @@ def test_ghost256_grid_visits_every_job_once(jobs):
             visits.append(job)
             job += grid
     assert sorted(visits) == list(range(jobs))
+
+
+# ------------------------ 384x256-tile clip kernel, ragged last row tile (tgemm_wide_kernel)
+#
+# A row tile covers 384 columns of G (output rows). In the last row tile of a
+# d_out that is a multiple of 32 but not of 384, a lane's G copy reads column
+# block min(blk, nvb - 1) of its k-row (blk 0..11, 32 columns each), and the
+# store skips the 32-row blocks at or past nvb.
+
+def wide_tile_rule(T, d_in, d_out, cus=256):
+    tiles_m = -(-d_out // 384)
+    pad = tiles_m * 384 - d_out
+    ragged = d_out % 32 == 0 and 50 * pad <= 3 * d_out and tiles_m * (d_in // 256) >= cus
+    return d_in % 256 == 0 and T % 64 == 0 and (d_out % 384 == 0 or ragged)
+
+
+@pytest.mark.parametrize("M", [384, 736, 4064, 11008, 4096])
+def test_wide_ragged_row_tile_copies_stay_in_bounds(M):
+    assert wide_tile_rule(64, 256 * 256, M)
+    tiles_m = -(-M // 384)
+    for tm in range(tiles_m):
+        nvb = min(12, (M - 384 * tm) // 32)
+        assert nvb >= 1
+        cols_read, rows_stored = set(), set()
+        for t in range(48):                      # the slot's G copies (16 waves x 3)
+            for lane in range(64):
+                l_unit, l_byte = lane >> 4, 16 * (lane & 3)
+                blk = 4 * (t % 3) + l_unit
+                byte = 384 * tm * 2 + 64 * min(blk, nvb - 1) + l_byte   # within one k-row of G
+                assert 0 <= byte and byte + 16 <= M * 2
+                cols_read.add(byte // 2 // 8)
+        for wave in range(16):
+            wm = wave // 4
+            for i in range(3):
+                if wm * 3 + i >= nvb:
+                    continue
+                for r in range(32):
+                    rows_stored.add(384 * tm + 32 * (wm * 3 + i) + r)
+        assert rows_stored == set(range(384 * tm, min(384 * (tm + 1), M)))
+        # every valid 8-column group of the tile is read
+        assert {c for c in cols_read} >= set(range(384 * tm // 8, min(384 * (tm + 1), M) // 8))
+
+
+@pytest.mark.parametrize("d_in,d_out,ok", [(256, 384, True), (4096, 11008, True), (6144, 4064, True),
+                                           (4096, 4096, False), (65536, 4096, True),
+                                           (65536, 512, False), (65536, 416, False), (256, 736, False)])
+def test_wide_tile_rule(d_in, d_out, ok):
+    """Whole row tiles always; a ragged last row tile only with at most 6 %
+    padding and at least one tile per CU (256)."""
+    assert wide_tile_rule(64, d_in, d_out) == ok
