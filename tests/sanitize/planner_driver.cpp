@@ -79,6 +79,18 @@ int main() {
   queries({shape(2, 37, 13, 21, BF, 0), shape(2, 37, 1, 33, BF, 1), shape(2, 37, 33, 1, BF, 2)});
   queries({shape(8, 128, 768, 4, F, 0), shape(8, 128, 4, 2304, F, 1)});        // adapters
   queries({shape(1 << 20, 1, 4, 4, F, 0)});                                    // many examples
+  // Gram form on 256-row tiles: the park area (256 KB per workgroup) and the
+  // grid cap of 512 workgroups (200 x 6 = 1200 jobs).
+  const dpsgd_layer c4base = shape(16, 1024, 4096, 11008, BF, 0);
+  CHECK(dpsgd_norms_workspace_bytes(&c4base, 1, DPSGD_NORM_GHOST) >= (size_t)160 * 262144);
+  const dpsgd_layer capped = shape(200, 520, 64, 64, BF, 0);
+  CHECK(dpsgd_norms_workspace_bytes(&capped, 1, DPSGD_NORM_GHOST) == 4864 + (size_t)512 * 262144);
+  queries({capped, shape(200, 300, 128, 64, BF, 1)});
+  // Ragged last row tiles of the 384x256 clip kernel, with a split tail, and
+  // a 4096 x 4096 layer (one round of 256x256 tiles).
+  queries({shape(1, 128, 6144, 4064, BF, 0)});
+  queries({shape(2, 64, 6144, 4064, BF, 0)});
+  queries({shape(16, 1024, 4096, 4096, BF, 0)});
   if (failures) {
     std::fprintf(stderr, "%d checks failed\n", failures);
     return 1;
