@@ -106,8 +106,9 @@ typedef struct dpsgd_layer {
  *             contents on entry do not matter and are clobbered. It holds
  *             per-example partials and, when a bf16 layer with T > 256 and
  *             widths that are multiples of 64 runs the Gram form, a park
- *             area of 256 KB per workgroup of that kernel (at most 512
- *             workgroups: 128 MB).
+ *             area of at most 128 MB (256 KB per workgroup of that kernel,
+ *             or, when few tiles are split along the columns, two 256 KB
+ *             partial tiles per part).
  * T = 1 layers always use the closed form ||a||^2 ||g||^2 whatever the mode.
  * ------------------------------------------------------------------------- */
 size_t dpsgd_norms_workspace_bytes(const dpsgd_layer* layers, int32_t n_layers, int32_t mode);

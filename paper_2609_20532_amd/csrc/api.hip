@@ -68,17 +68,25 @@ NormForm planned_form(const dpsgd_layer& L, NormForm f, bool park_ok) {
   return f == FORM_GHOST && park_ok && ghost256_ok(L) ? FORM_GHOST256 : f;
 }
 
-// Fills cols, P, park_off and bytes from forms.
+// Fills cols, P, park_off and bytes from forms. The park area is the largest
+// that a launch of 256-row tiles needs, grouped as the norm launcher groups
+// the layers (up to 256 layers per group, in order).
 void finish_norm_plan(const dpsgd_layer* layers, int32_t n, NormPlan* p) {
-  int64_t jobs256 = 0;
   p->P = 0;
   for (int32_t l = 0; l < n; ++l) {
     p->cols[l] = p->P;
     p->P += norm_partials_per_example(layers[l], p->forms[l]);
-    if (p->forms[l] == FORM_GHOST256) jobs256 += layers[l].B * ghost256_pairs(layers[l]);
+  }
+  size_t park = 0;
+  std::vector<int> idx;
+  for (int32_t base = 0; base < n; base += 256) {
+    idx.clear();
+    for (int32_t l = base; l < n && l < base + 256; ++l)
+      if (p->forms[l] == FORM_GHOST256) idx.push_back(l);
+    if (!idx.empty()) park = std::max(park, ghost256_park_bytes(layers, idx.data(), (int)idx.size()));
   }
   p->park_off = round_up((size_t)layers[0].B * (size_t)p->P * sizeof(float), 256);
-  p->bytes = p->park_off + (jobs256 > 0 ? ghost256_park_bytes(jobs256) : 0);
+  p->bytes = p->park_off + park;
 }
 
 NormPlan plan_norms(const dpsgd_layer* layers, int32_t n, int32_t mode, bool park_ok) {

@@ -28,6 +28,8 @@
 // 128-byte lines). Otherwise every tile has its own four-wave workgroup (2 x 2
 // grid of 64 x 64 sub-tiles, two workgroups per CU), and the tiles of one
 // example run on one XCD so the rows they share come from its L2.
+#include <algorithm>
+
 #include "lds_dma.h"
 #include "mma.h"
 
@@ -451,18 +453,30 @@ struct G4Cfg {
   }
 };
 
+// split == 1: job = tile; park holds kG4ParkFloats per workgroup of the grid.
+// split > 1: job = (tile, part), part p taking slices [n p / split,
+// n (p + 1) / split) of the tile's n = (d_in + d_out) / 64 column slices (A's
+// first, then G's); park holds two slots of kG4ParkFloats per job (its
+// partial GA, masked to the tile's valid rows and columns, and its partial
+// GG), which ghost256_combine_kernel adds and multiplies.
 struct G4Args {
   GhEntry L[kMaxLayersPerLaunch];
   int32_t n;
+  int32_t split;
   uint32_t jobs;
   int64_t P;
   float* partials;
-  float* park;   // kG4ParkFloats per workgroup of the grid
+  float* park;
 };
 
-// sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] of 256 x 256 tile (p, q) of example i.
-template <int BK, int WAVES, bool DIAG>
-__device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* lds, float* park) {
+// sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] of 256 x 256 tile (p, q) of example
+// i over the column slices [s_lo, s_hi) (A's slices first, then G's), with
+// park a kG4ParkFloats scratch slot of this workgroup. SPLIT: the slices are
+// part of the tile; the partial GA (masked) goes to park_a and the partial GG
+// to park_g instead, and the result is 0.
+template <int BK, int WAVES, bool DIAG, bool SPLIT>
+__device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* lds, float* park,
+                               int s_lo_arg, int s_hi_arg, float* park_a, float* park_g) {
   using C = G4Cfg<BK, WAVES>;
   constexpr int MB = C::kMB, NB = C::kNB;
   const int lane = threadIdx.x & 63;
@@ -472,6 +486,8 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
   const int rows_p = min(kG4Rows, T - kG4Rows * p);
   const int rows_q = min(kG4Rows, T - kG4Rows * q);
   const int nA = E.d_in / BK, n = nA + E.d_out / BK;
+  // A whole tile runs every slice (bounds known to the compiler).
+  const int s_lo = SPLIT ? s_lo_arg : 0, s_hi = SPLIT ? s_hi_arg : n;
   const char* Ab = static_cast<const char*>(E.A) + i * (int64_t)T * E.d_in * 2;
   const char* Gb = static_cast<const char*>(E.G) + i * (int64_t)T * E.d_out * 2;
   const uint32_t lds0 = lds_address(lds);
@@ -525,7 +541,7 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
   __syncthreads();
 #pragma unroll
   for (int d = 0; d < C::kStages - 1; ++d)
-    if (d < n) issue(d, d);
+    if (s_lo + d < s_hi) issue(s_lo + d, d);
 
   auto slice = [&](int s) {
     // This wave's copies of slice s have landed once at most the later
@@ -533,15 +549,16 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
     // are outstanding too, so that wait is for everything); the barrier makes
     // every wave's part visible and guarantees slice s - 1, whose slot is
     // refilled next, is no longer read.
-    const int later = n - 1 - s;
+    const int later = s_hi - 1 - s;
     if (s == nA) wait_vmcnt<0>();
     else if (later >= C::kStages - 2) wait_vmcnt<kCopies * (C::kStages - 2)>();
     else if (later == 1) wait_vmcnt<kCopies>();
     else wait_vmcnt<0>();
     barrier_no_wait();
-    if (s + C::kStages - 1 < n) issue(s + C::kStages - 1, (s + C::kStages - 1) % C::kStages);
+    if (s + C::kStages - 1 < s_hi)
+      issue(s + C::kStages - 1, (s - s_lo + C::kStages - 1) % C::kStages);
     typedef __attribute__((address_space(3))) const bf16x8_t lds_frag;
-    const char* base = lds + (s % C::kStages) * C::kStageBytes;
+    const char* base = lds + ((s - s_lo) % C::kStages) * C::kStageBytes;
     // Operands of k step st + 1 are read while the MFMAs of step st run; the
     // scheduling barrier keeps the reads of later steps from being hoisted
     // further (which would hold every step's operands in registers at once).
@@ -568,20 +585,39 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
   // Park slot of this lane: float4 k (k = 4 (NB a + b) + c holds elements
   // 4 c .. 4 c + 3 of block (a, b)) at float offset kParkPerWave wave + 256 k +
   // 4 lane, so every store and load instruction covers 1 KB contiguously.
-  float* mine = park + C::kParkPerWave * (int)wave_u + 4 * lane;
-  for (int s = 0; s < nA; ++s) slice(s);
+  // Element v of block (a, b) in lane l: tile row 32 (MB wm + a) + 8 (v / 4) +
+  // 4 (l / 32) + v % 4, column 32 (NB wn + b) + l % 32.
+  const int lane_off = C::kParkPerWave * (int)wave_u + 4 * lane;
+  auto park_acc = [&](float* dst, bool masked) {
 #pragma unroll
-  for (int a = 0; a < MB; ++a)
+    for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
+      for (int b = 0; b < NB; ++b) {
+        const int col = 32 * (NB * wn + b) + (lane & 31);
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        *reinterpret_cast<f32x4_t*>(mine + 256 * (4 * (NB * a + b) + c)) =
-            f32x4_t{acc[a][b][4 * c], acc[a][b][4 * c + 1], acc[a][b][4 * c + 2], acc[a][b][4 * c + 3]};
-      acc[a][b] = f32x16_t{};
-      __builtin_amdgcn_sched_barrier(0);   // one block's values in flight at a time
-    }
-  for (int s = nA; s < n; ++s) slice(s);
+        for (int c = 0; c < 4; ++c) {
+          f32x4_t v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int row = 32 * (MB * wm + a) + 8 * c + 4 * g + e;
+            const float x = acc[a][b][4 * c + e];
+            v4[e] = !masked || (row < rows_p && col < rows_q) ? x : 0.f;
+          }
+          *reinterpret_cast<f32x4_t*>(dst + lane_off + 256 * (4 * (NB * a + b) + c)) = v4;
+        }
+        acc[a][b] = f32x16_t{};
+        __builtin_amdgcn_sched_barrier(0);   // one block's values in flight at a time
+      }
+  };
+  const int a_end = min(s_hi, nA);
+  for (int s = s_lo; s < a_end; ++s) slice(s);
+  if (s_lo < nA) park_acc(SPLIT ? park_a : park, SPLIT);
+  for (int s = max(s_lo, nA); s < s_hi; ++s) slice(s);
+  if constexpr (SPLIT) {
+    if (s_hi > nA) park_acc(park_g, false);
+    return 0.f;
+  }
+  float* mine = park + lane_off;
 
   // Element v of block (a, b) in lane l: tile row 32 (MB wm + a) + 8 (v / 4) +
   // 4 (l / 32) + v % 4, column 32 (NB wn + b) + l % 32. A diagonal tile is
@@ -609,36 +645,56 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
   return sum;
 }
 
-template <int BK, int WAVES>
+// Layer of a job (the last layer starting at or before it).
+__device__ __forceinline__ int g4_find_layer(const G4Args& args, uint32_t job) {
+  int lo = 0, hi = args.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (args.L[mid].wg_begin <= job) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Tile pr of the upper triangle of an nt x nt block grid (row-major order).
+__device__ __forceinline__ void g4_tile_pq(int nt, int pr, int& p, int& q) {
+  p = 0;
+  while (pr >= nt - p) {
+    pr -= nt - p;
+    ++p;
+  }
+  q = p + pr;
+}
+
+// SPLIT: the launch's tiles are split into args.split parts (a separate
+// instantiation, so that the whole-tile kernel's code is not shared with it).
+template <int BK, int WAVES, bool SPLIT>
 __global__ __launch_bounds__(64 * WAVES, 1) void ghost_tile256_kernel(G4Args args) {
   __shared__ __attribute__((aligned(1024))) char lds[G4Cfg<BK, WAVES>::kLdsBytes];
   float* park = args.park + (size_t)blockIdx.x * kG4ParkFloats;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // Consecutive logical indices (the tiles of one example) run on one XCD, so
-  // the rows that two tiles share are fetched from HBM into that XCD's L2 once.
+  const int S = SPLIT ? args.split : 1;
+  // Consecutive logical indices (the tiles of one example, and the parts of
+  // one tile) run on one XCD, so the rows that they share are fetched from HBM
+  // into that XCD's L2 once.
   for (uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x); job < args.jobs; job += gridDim.x) {
-    int l = 0;
-    {
-      int lo = 0, hi = args.n - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (args.L[mid].wg_begin <= job) lo = mid; else hi = mid - 1;
-      }
-      l = lo;
-    }
-    const GhEntry& E = args.L[l];
+    const GhEntry& E = args.L[g4_find_layer(args, job)];
     const uint32_t w = job - E.wg_begin;
-    const int64_t i = w / (uint32_t)E.pairs;
-    int pr = (int)(w % (uint32_t)E.pairs);
-    const int pr0 = pr;
-    int p = 0;
-    while (pr >= E.nt - p) {
-      pr -= E.nt - p;
-      ++p;
+    const uint32_t tile = w / (uint32_t)S;
+    const int part = (int)(w % (uint32_t)S);
+    const int64_t i = tile / (uint32_t)E.pairs;
+    const int pr = (int)(tile % (uint32_t)E.pairs);
+    int p, q;
+    g4_tile_pq(E.nt, pr, p, q);
+    const int n = (E.d_in + E.d_out) / BK;
+    if constexpr (SPLIT) {
+      const int s_lo = (int)((int64_t)n * part / S), s_hi = (int)((int64_t)n * (part + 1) / S);
+      float* pa = args.park + (size_t)job * 2 * kG4ParkFloats;
+      if (p == q) ghost_tile256<BK, WAVES, true, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats);
+      else ghost_tile256<BK, WAVES, false, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats);
+      continue;
     }
-    const int q = p + pr;
-    float s = p == q ? ghost_tile256<BK, WAVES, true>(E, i, p, q, lds, park)
-                     : 2.0f * ghost_tile256<BK, WAVES, false>(E, i, p, q, lds, park);
+    float s = p == q ? ghost_tile256<BK, WAVES, true, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr)
+                     : 2.0f * ghost_tile256<BK, WAVES, false, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr);
     s = wave_sum(s);
     __syncthreads();   // the ring is free again
     float* red = reinterpret_cast<float*>(lds);
@@ -648,8 +704,76 @@ __global__ __launch_bounds__(64 * WAVES, 1) void ghost_tile256_kernel(G4Args arg
       float v = 0.f;
 #pragma unroll
       for (int k = 0; k < WAVES; k += 2) v += red[k] + red[k + 1];
-      args.partials[i * args.P + E.partial_col + pr0] = v;
+      args.partials[i * args.P + E.partial_col + pr] = v;
     }
+  }
+}
+
+// Split tiles: one workgroup per tile adds the parts' partial Gram tiles in
+// part order and writes (p == q ? 1 : 2) sum GA GG (GA is zero outside the
+// tile's valid rows and columns). The parked positions of every part follow
+// the same lane layout, so the product is elementwise over the slots. Each of
+// the 1024 threads takes 16 float4 positions, loaded four at a time from
+// every slot before they are multiplied (the pass is bound by load latency).
+constexpr int kCbThreads = 1024;
+template <int S>
+__global__ __launch_bounds__(kCbThreads) void ghost256_combine_kernel(G4Args args) {
+  __shared__ float red[kCbThreads / 64];
+  const uint32_t job0 = blockIdx.x * (uint32_t)S;   // part 0 of this tile
+  const GhEntry& E = args.L[g4_find_layer(args, job0)];
+  const uint32_t tile = (job0 - E.wg_begin) / (uint32_t)S;
+  const int64_t i = tile / (uint32_t)E.pairs;
+  const int pr = (int)(tile % (uint32_t)E.pairs);
+  int p, q;
+  g4_tile_pq(E.nt, pr, p, q);
+  const int nA = E.d_in / kG4BK, n = nA + E.d_out / kG4BK;
+  const float* base = args.park + (size_t)job0 * 2 * kG4ParkFloats;
+  // The parts holding A slices are a prefix (parts 0 .. pa - 1), those holding
+  // G slices a suffix (pg .. S - 1). Every load is issued unconditionally from
+  // a slot that was written (the part index clamped into the prefix or the
+  // suffix), and a select keeps only the parts' own slots, so the loads of a
+  // batch are all in flight at once.
+  int pa = 0, pg = S;
+#pragma unroll
+  for (int part = 0; part < S; ++part) {
+    if ((int64_t)n * part / S < nA) pa = part + 1;
+    if ((int64_t)n * (part + 1) / S > nA && pg == S) pg = part;
+  }
+  constexpr int kIters = kG4ParkFloats / (4 * kCbThreads);   // 16
+  constexpr int kBatch = 4;
+  float sum = 0.f;
+  for (int k0 = 0; k0 < kIters; k0 += kBatch) {
+    f32x4_t ga[kBatch], gg[kBatch];
+#pragma unroll
+    for (int kk = 0; kk < kBatch; ++kk) ga[kk] = gg[kk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int part = 0; part < S; ++part) {
+      const float* sa = base + (size_t)min(part, pa - 1) * 2 * kG4ParkFloats;
+      const float* sg = base + (size_t)max(part, pg) * 2 * kG4ParkFloats + kG4ParkFloats;
+      const bool use_a = part < pa, use_g = part >= pg;
+#pragma unroll
+      for (int kk = 0; kk < kBatch; ++kk) {
+        const int pos = 4 * ((k0 + kk) * kCbThreads + (int)threadIdx.x);
+        const f32x4_t va = *reinterpret_cast<const f32x4_t*>(sa + pos);
+        const f32x4_t vg = *reinterpret_cast<const f32x4_t*>(sg + pos);
+        const f32x4_t z = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        ga[kk] += use_a ? va : z;
+        gg[kk] += use_g ? vg : z;
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < kBatch; ++kk)
+      sum += (ga[kk][0] * gg[kk][0] + ga[kk][1] * gg[kk][1]) + (ga[kk][2] * gg[kk][2] + ga[kk][3] * gg[kk][3]);
+  }
+  sum = wave_sum(sum);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kCbThreads / 64; w += 2) v += red[w] + red[w + 1];
+    args.partials[i * args.P + E.partial_col + pr] = p == q ? v : 2.0f * v;
   }
 }
 
@@ -662,22 +786,73 @@ bool ghost_dma_ok(const dpsgd_layer& L) {
 
 bool ghost256_ok(const dpsgd_layer& L) { return L.T > kG4Rows && ghost_dma_ok(L); }
 
+// Park floats of an unsplit launch: one slot per workgroup of the capped grid.
+static size_t ghost256_park_floats_per_grid(int64_t jobs) {
+  const int64_t grid = jobs < kGhost256MaxGrid ? jobs : kGhost256MaxGrid;
+  return (size_t)grid * kG4ParkFloats;
+}
+
 int64_t ghost256_pairs(const dpsgd_layer& L) {
   const int64_t nt = ceil_div(L.T, kG4Rows);
   return nt * (nt + 1) / 2;
 }
 
-size_t ghost256_park_bytes(int64_t jobs) {
-  const int64_t grid = jobs < kGhost256MaxGrid ? jobs : kGhost256MaxGrid;
-  return (size_t)grid * kG4ParkFloats * sizeof(float);
+namespace {
+
+// Split plan of one launch of 256-row tiles (at most kMaxLayersPerLaunch
+// layers). A job runs on one CU and a tile's time is set by its column
+// slices, so with fewer tiles than CUs the chip idles; splitting every tile's
+// slices into S parts (at least 16 slices each) runs S times as many shorter
+// jobs, at the cost of parking about S + 1 partial Gram tiles per tile for a
+// combine pass. S is the largest (at most 4) whose jobs still fit one round
+// on the CUs: with a second round the per-slice time rises by about a third
+// when every CU copies at once and the parked traffic grows, and the split
+// measured slower (c4's shape, B T = 32768: 0.79 against 0.71 ms), while
+// within one round it measured 1.2-2.6 times faster (B T = 1024 ... 12288).
+struct G4Plan {
+  int split = 1;
+  int64_t tiles = 0;
+  size_t park_bytes = 0;
+};
+
+G4Plan plan_ghost256(const dpsgd_layer* layers, const int* idx, int n, int64_t cus) {
+  G4Plan plan;
+  int64_t slices = 0;
+  for (int k = 0; k < n; ++k) {
+    const dpsgd_layer& L = layers[idx[k]];
+    plan.tiles += L.B * ghost256_pairs(L);
+    slices = std::max<int64_t>(slices, (L.d_in + L.d_out) / kG4BK);
+  }
+  for (int S = 4; S >= 2; --S)
+    if (plan.tiles * S <= cus && slices / S >= 16) {
+      plan.split = S;
+      break;
+    }
+  plan.park_bytes = plan.split == 1
+                        ? ghost256_park_floats_per_grid(plan.tiles) * sizeof(float)
+                        : (size_t)plan.tiles * plan.split * 2 * kG4ParkFloats * sizeof(float);
+  return plan;
+}
+
+}  // namespace
+
+size_t ghost256_park_bytes(const dpsgd_layer* layers, const int* idx, int n) {
+  size_t bytes = 0;
+  for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
+    const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    bytes = std::max(bytes, plan_ghost256(layers, idx + base, m, tr_cu_count()).park_bytes);
+  }
+  return bytes;
 }
 
 int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                     float* partials, int64_t P, float* park, hipStream_t stream) {
   for (int base = 0; base < n; base += kMaxLayersPerLaunch) {
     const int m = n - base < kMaxLayersPerLaunch ? n - base : kMaxLayersPerLaunch;
+    const G4Plan plan = plan_ghost256(layers, idx + base, m, tr_cu_count());
     G4Args a{};
     a.n = m;
+    a.split = plan.split;
     a.P = P;
     a.partials = partials;
     a.park = park;
@@ -695,16 +870,27 @@ int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int6
       E.partial_col = (int32_t)cols[idx[base + k]];
       E.wg_begin = (uint32_t)jobs;
       a.L[k] = E;
-      jobs += L.B * (int64_t)E.pairs;
+      jobs += L.B * (int64_t)E.pairs * plan.split;
     }
     if (jobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
     a.jobs = (uint32_t)jobs;
     // The launches of one call run in stream order, so they share the park
-    // area (sized for the largest grid).
+    // area (sized for the largest plan).
     const int64_t grid = jobs < kGhost256MaxGrid ? jobs : kGhost256MaxGrid;
-    hipLaunchKernelGGL((ghost_tile256_kernel<kG4BK, kG4Waves>), dim3((uint32_t)grid),
-                       dim3(64 * kG4Waves), 0, stream, a);
+    if (plan.split > 1)
+      hipLaunchKernelGGL((ghost_tile256_kernel<kG4BK, kG4Waves, true>), dim3((uint32_t)grid),
+                         dim3(64 * kG4Waves), 0, stream, a);
+    else
+      hipLaunchKernelGGL((ghost_tile256_kernel<kG4BK, kG4Waves, false>), dim3((uint32_t)grid),
+                         dim3(64 * kG4Waves), 0, stream, a);
     if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    if (plan.split > 1) {
+      auto combine = plan.split == 2 ? ghost256_combine_kernel<2>
+                     : plan.split == 3 ? ghost256_combine_kernel<3>
+                                       : ghost256_combine_kernel<4>;
+      hipLaunchKernelGGL(combine, dim3((uint32_t)plan.tiles), dim3(kCbThreads), 0, stream, a);
+      if (check_launch() != DPSGD_OK) return DPSGD_ERR_HIP;
+    }
   }
   return DPSGD_OK;
 }

@@ -57,6 +57,14 @@ def test_workspace_queries_and_mode_selection(lib):
     # More than 512 jobs: the grid (and the park area) stays at 512 workgroups.
     big = dpsgd.shape_layer(200, 520, 64, 64)    # 3 row blocks, 6 pairs, 1200 jobs
     assert dpsgd.dpsgd_norms_workspace_bytes(big, dpsgd.DPSGD_NORM_GHOST) == 4864 + 512 * 262144
+    # c4's 11008-wide layer: 160 tiles of 236 column slices; splitting them
+    # would need a second round on 256 CUs, so they stay whole.
+    c4 = dpsgd.shape_layer(16, 1024, 4096, 11008)
+    assert dpsgd.dpsgd_norms_workspace_bytes(c4, dpsgd.DPSGD_NORM_GHOST) == 768 + 160 * 262144
+    # At B = 8 (80 tiles) each tile is split into 3 column parts (240 jobs, one
+    # round) that park their partial Gram tiles: two 256 KB slots per part.
+    c4b8 = dpsgd.shape_layer(8, 1024, 4096, 11008)
+    assert dpsgd.dpsgd_norms_workspace_bytes(c4b8, dpsgd.DPSGD_NORM_GHOST) == 512 + 80 * 3 * 2 * 262144
     # float32 keeps the 128-row tiles (4 T-tiles -> 10 pairs) and no park area.
     c3f = dpsgd.shape_layer(64, 512, 768, 3072, dpsgd.DPSGD_F32)
     assert dpsgd.dpsgd_norms_workspace_bytes(c3f, dpsgd.DPSGD_NORM_GHOST) == 2560

@@ -2,10 +2,13 @@
 
 Per-example squared norms ||G_i^T A_i||_F^2 (Section 2.2's clipping norm) of
 bf16 layers with T > 256 run one 256 x 256 tile of the T x T upper triangle
-per workgroup, parking the activation Gram tile in the workspace. Cases: layers
-of different T in one launch, more jobs than the capped grid (workgroups take
-several jobs and reuse their park slot), the fused clipped-sum call, and
-agreement with the 128-row-tile kernel of the allocation-free call.
+per workgroup, parking the activation Gram tile in the workspace; with few
+tiles and long rows every tile's columns are split into parts whose partial
+Gram tiles a combine pass adds. Cases: layers of different T in one launch,
+split tiles (a part with only A's columns, a part across the A/G boundary),
+more jobs than the capped grid (workgroups take several jobs and reuse their
+park slot), the fused clipped-sum call, and agreement with the 128-row-tile
+kernel of the allocation-free call.
 """
 
 import sys
@@ -58,6 +61,12 @@ CASES = [
     (3, [(300, 64, 128), (700, 128, 64), (1024, 64, 192), (257, 192, 64)]),
     (2, [(512, 768, 256)]),        # two full row blocks, three tiles
     (1, [(777, 64, 64)]),          # four row blocks, the last of 9 rows
+    # Few tiles with long rows: each tile's 64 column slices are split into 4
+    # parts (the first covers exactly A's 16), combined in a second pass.
+    (1, [(512, 1024, 3072)]),
+    # 10 tiles of a ragged T in 3 parts of 16, 16 and 17 slices; the middle part
+    # holds A's last 8 and G's first 8.
+    (1, [(777, 1536, 1600)]),
 ]
 
 

@@ -515,3 +515,34 @@ def test_wide_tile_rule(d_in, d_out, ok):
     """Whole row tiles always; a ragged last row tile only with at most 6 %
     padding and at least one tile per CU (256)."""
     assert wide_tile_rule(64, d_in, d_out) == ok
+
+
+@pytest.mark.parametrize("n,nA,S", [(236, 64, 3), (64, 16, 4), (49, 24, 3), (60, 12, 1), (17, 1, 1)])
+def test_ghost256_split_parts_cover_the_slices(n, nA, S):
+    """Part p of a split tile takes slices [n p / S, n (p + 1) / S); the
+    combine adds GA over the parts that hold A slices (lo < nA) and GG over
+    those that hold G slices (hi > nA): every slice once, in part order."""
+    seen = []
+    a_parts, g_parts = [], []
+    for p in range(S):
+        lo, hi = n * p // S, n * (p + 1) // S
+        assert lo < hi
+        seen.extend(range(lo, hi))
+        if lo < nA:
+            a_parts.append(p)
+        if hi > nA:
+            g_parts.append(p)
+    assert seen == list(range(n))
+    assert sorted({s for p in a_parts for s in range(n * p // S, n * (p + 1) // S) if s < nA}) \
+        == list(range(nA))
+    assert sorted({s for p in g_parts for s in range(n * p // S, n * (p + 1) // S) if s >= nA}) \
+        == list(range(nA, n))
+    # The combine's clamping: A parts are the prefix 0 .. pa - 1, G parts the
+    # suffix pg .. S - 1; part p reads A slot min(p, pa - 1) and G slot
+    # max(p, pg), always written, and keeps them only when it owns them.
+    pa = max(p + 1 for p in range(S) if n * p // S < nA)
+    pg = min(p for p in range(S) if n * (p + 1) // S > nA)
+    assert a_parts == list(range(pa)) and g_parts == list(range(pg, S))
+    for p in range(S):
+        assert min(p, pa - 1) in a_parts and max(p, pg) in g_parts
+        assert (p < pa) == (p in a_parts) and (p >= pg) == (p in g_parts)
