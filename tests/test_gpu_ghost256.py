@@ -91,6 +91,20 @@ def test_ghost256_norms_match_the_oracle(dp, case):
     _log(f"case {case}: oracle error {err:.2e}, 128-row tiles {rel:.2e}")
 
 
+def test_ghost256_more_layers_than_one_launch(dp):
+    """50 T > 256 layers: two launches (48 layers, then 2) share the park area."""
+    B = 2
+    dims = [(300 + 8 * (k % 5), 64, 64) for k in range(50)]
+    _log(f"[gpu] ghost256 two launches: B={B}, {len(dims)} layers")
+    hs = [_host_layer(B, T, di, do, seed=500 + k, tensor_id=k) for k, (T, di, do) in enumerate(dims)]
+    dev = device_layers(hs)
+    Ls = [d[0] for d in dev]
+    got = _norms(dp, Ls, dp.DPSGD_NORM_GHOST)
+    err = _norm_err(got, hs)
+    assert err <= NORM_TOL, f"norm error {err:.2e}"
+    _log(f"two launches: oracle error {err:.2e}")
+
+
 def test_ghost256_more_jobs_than_the_grid(dp):
     """1200 tile jobs on a grid of 512 workgroups: each workgroup takes two or
     three jobs and reuses its park slot; two calls give identical bits."""

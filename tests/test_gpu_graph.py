@@ -46,6 +46,9 @@ CASES = [
     ("bf16 kernels", 4, wl.BF16, [(256, 256, 384), (256, 256, 512), (256, 40, 24), (300, 64, 128)],
      False),
     ("fused, adapters", 8, wl.F32, [(128, 768, 4), (128, 4, 2304), (128, 96, 80)], True),
+    # A T > 256 bf16 Gram layer with few tiles: its column slices split into 4
+    # parts whose partial Gram tiles a combine kernel adds, inside the graph.
+    ("bf16 split Gram tiles", 1, wl.BF16, [(512, 1024, 3072)], False),
 ]
 
 
