@@ -67,6 +67,9 @@ CASES = [
     # 10 tiles of a ragged T in 3 parts of 16, 16 and 17 slices; the middle part
     # holds A's last 8 and G's first 8.
     (1, [(777, 1536, 1600)]),
+    # One launch split in 4 parts for the large layer; the small layer's 2
+    # slices leave two of its parts empty.
+    (1, [(512, 2048, 2048), (300, 64, 64)]),
 ]
 
 
@@ -82,7 +85,9 @@ def test_ghost256_norms_match_the_oracle(dp, case):
     got = _norms(dp, Ls, dp.DPSGD_NORM_GHOST)
     err = _norm_err(got, hs)
     assert err <= NORM_TOL, f"norm error {err:.2e}"
-    # The allocation-free call takes the 128-row tiles: same sums, another order.
+    # The allocation-free call takes the 128-row tiles: same sums, another
+    # order. On these seeded inputs both often land on the same float32 bits;
+    # on others they differ by a few ulp, well inside the bound.
     tiles128 = torch.full((B,), 5.0, dtype=torch.float32, device="cuda")
     dp.dpsgd_per_example_norms_multi_noalloc(Ls, dp.DPSGD_NORM_GHOST, tiles128)
     torch.cuda.synchronize()
