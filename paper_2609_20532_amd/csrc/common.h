@@ -115,14 +115,16 @@ int launch_gram64(const dpsgd_layer* layers, const int* idx, int n, const int64_
 int launch_ghost_dma(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                      float* partials, int64_t P, hipStream_t stream);
 // Gram-form norms on 256-row tiles (ghost.hip): ghost_dma_ok layers with
-// T > 256, ghost256_pairs partials per example. At most kGhost256MaxGrid
-// workgroups run. A launch either keeps whole tiles (each workgroup parks a
-// 256 KB float32 tile) or splits every tile's columns into parts that park
-// their partial Gram tiles for a combine pass; ghost256_park_bytes: the park
-// area of launch_ghost256 over the layers idx[0..n) (the largest launch).
+// T > 256, ghost256_cols partials per example (nt^2 for nt row blocks: one
+// per diagonal tile, two per off-diagonal tile). At most kGhost256MaxGrid
+// workgroups run. A launch keeps whole tiles, runs its off-diagonal tiles as
+// two row halves (each workgroup parks a 256 KB float32 tile), or splits
+// every tile's columns into parts that park their partial Gram tiles for a
+// combine pass; ghost256_park_bytes: the park area of launch_ghost256 over
+// the layers idx[0..n) (the largest launch).
 constexpr int64_t kGhost256MaxGrid = 512;
 bool ghost256_ok(const dpsgd_layer& L);
-int64_t ghost256_pairs(const dpsgd_layer& L);
+int64_t ghost256_cols(const dpsgd_layer& L);
 size_t ghost256_park_bytes(const dpsgd_layer* layers, const int* idx, int n);
 int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int64_t* cols,
                     float* partials, int64_t P, float* park, hipStream_t stream);

@@ -54,7 +54,8 @@ struct GhEntry {
   int32_t partial_col;
   int32_t groups;      // nt / 2 three-tile groups
   int32_t singles;     // pairs - 3 groups tiles outside them
-  int32_t pad;
+  int32_t jpe;         // 256-row tiles: jobs per example of a launch without a split
+  int32_t halves;      // 256-row tiles: off-diagonal tiles run as two row halves
 };
 struct GhArgs {
   GhEntry L[kMaxLayersPerLaunch];
@@ -422,7 +423,12 @@ __global__ __launch_bounds__(kGgThreads, 1) void ghost_group_kernel(GhArgs args)
 // read back only by that lane), GG reuses the same registers, and the lanes
 // read GA back for the elementwise product. WAVES waves form a (WAVES / 2) x 2
 // grid of sub-tiles of kMB x 4 blocks of 32 x 32: 64 x 128 for eight waves,
-// 128 x 128 for four. The grid is capped at
+// 128 x 128 for four. A diagonal tile is symmetric, so its two sub-tiles
+// below the 128-row diagonal are skipped and the two above it count twice;
+// an off-diagonal tile may run as two jobs, one per 128-row half of block p
+// (the four waves of that half multiply, all eight copy and synchronise).
+// The loop is bound by LDS bandwidth, so what such a skipped sub-tile saves
+// is mostly its operand reads. The grid is capped at
 // kGhost256MaxGrid workgroups, each with a park slot of its own; workgroup b
 // takes jobs b, b + grid, ... .
 
@@ -476,11 +482,15 @@ struct G4Args {
 // to park_g instead, and the result is 0.
 template <int BK, int WAVES, bool DIAG, bool SPLIT>
 __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* lds, float* park,
-                               int s_lo_arg, int s_hi_arg, float* park_a, float* park_g) {
+                               int s_lo_arg, int s_hi_arg, float* park_a, float* park_g,
+                               uint32_t act_mask, uint32_t w2_mask) {
   using C = G4Cfg<BK, WAVES>;
   constexpr int MB = C::kMB, NB = C::kNB;
   const int lane = threadIdx.x & 63;
   const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // A wave outside act_mask still copies and takes part in every barrier but
+  // reads no operands and multiplies nothing (its sub-tile adds 0).
+  const bool active = SPLIT || ((act_mask >> wave_u) & 1u) != 0u;
   const int wm = (int)(wave_u >> 1), wn = (int)(wave_u & 1u);
   const int T = E.T;
   const int rows_p = min(kG4Rows, T - kG4Rows * p);
@@ -557,6 +567,7 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
     barrier_no_wait();
     if (s + C::kStages - 1 < s_hi)
       issue(s + C::kStages - 1, (s - s_lo + C::kStages - 1) % C::kStages);
+    if (!active) return;
     typedef __attribute__((address_space(3))) const bf16x8_t lds_frag;
     const char* base = lds + ((s - s_lo) % C::kStages) * C::kStageBytes;
     // Operands of k step st + 1 are read while the MFMAs of step st run; the
@@ -611,12 +622,13 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
   };
   const int a_end = min(s_hi, nA);
   for (int s = s_lo; s < a_end; ++s) slice(s);
-  if (s_lo < nA) park_acc(SPLIT ? park_a : park, SPLIT);
+  if (s_lo < nA && active) park_acc(SPLIT ? park_a : park, SPLIT);
   for (int s = max(s_lo, nA); s < s_hi; ++s) slice(s);
   if constexpr (SPLIT) {
     if (s_hi > nA) park_acc(park_g, false);
     return 0.f;
   }
+  if (!active) return 0.f;
   float* mine = park + lane_off;
 
   // Element v of block (a, b) in lane l: tile row 32 (MB wm + a) + 8 (v / 4) +
@@ -642,7 +654,7 @@ __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* 
       sum += blk;
       __builtin_amdgcn_sched_barrier(0);   // one block's parked values in flight at a time
     }
-  return sum;
+  return ((w2_mask >> wave_u) & 1u) ? 2.0f * sum : sum;
 }
 
 // Layer of a job (the last layer starting at or before it).
@@ -665,6 +677,26 @@ __device__ __forceinline__ void g4_tile_pq(int nt, int pr, int& p, int& q) {
   q = p + pr;
 }
 
+// Off-diagonal tile o (row-major over p < q) of an nt x nt block grid, and
+// the inverse.
+__device__ __forceinline__ void g4_off_pq(int nt, int o, int& p, int& q) {
+  p = 0;
+  while (o >= nt - 1 - p) {
+    o -= nt - 1 - p;
+    ++p;
+  }
+  q = p + 1 + o;
+}
+__device__ __forceinline__ int g4_off_index(int nt, int p, int q) {
+  return p * (nt - 1) - p * (p - 1) / 2 + (q - p - 1);
+}
+
+// Waves of a diagonal tile: sub-tiles (wm, wn) = (wave / 2, wave % 2) cover
+// rows 64 wm .. +63 and columns 128 wn .. +127. The tile is symmetric: the two
+// sub-tiles below its 128-row diagonal (waves 4, 6) are skipped and the two
+// above it (waves 1, 3) count twice.
+constexpr uint32_t kG4DiagAct = 0xAFu, kG4DiagW2 = 0x0Au;
+
 // SPLIT: the launch's tiles are split into args.split parts (a separate
 // instantiation, so that the whole-tile kernel's code is not shared with it).
 template <int BK, int WAVES, bool SPLIT>
@@ -679,22 +711,46 @@ __global__ __launch_bounds__(64 * WAVES, 1) void ghost_tile256_kernel(G4Args arg
   for (uint32_t job = xcd_logical_index(blockIdx.x, gridDim.x); job < args.jobs; job += gridDim.x) {
     const GhEntry& E = args.L[g4_find_layer(args, job)];
     const uint32_t w = job - E.wg_begin;
-    const uint32_t tile = w / (uint32_t)S;
-    const int part = (int)(w % (uint32_t)S);
-    const int64_t i = tile / (uint32_t)E.pairs;
-    const int pr = (int)(tile % (uint32_t)E.pairs);
-    int p, q;
-    g4_tile_pq(E.nt, pr, p, q);
     const int n = (E.d_in + E.d_out) / BK;
+    int p, q;
     if constexpr (SPLIT) {
+      const uint32_t tile = w / (uint32_t)S;
+      const int part = (int)(w % (uint32_t)S);
+      const int64_t i = tile / (uint32_t)E.pairs;
+      g4_tile_pq(E.nt, (int)(tile % (uint32_t)E.pairs), p, q);
       const int s_lo = (int)((int64_t)n * part / S), s_hi = (int)((int64_t)n * (part + 1) / S);
       float* pa = args.park + (size_t)job * 2 * kG4ParkFloats;
-      if (p == q) ghost_tile256<BK, WAVES, true, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats);
-      else ghost_tile256<BK, WAVES, false, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats);
+      if (p == q) ghost_tile256<BK, WAVES, true, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats, 0u, 0u);
+      else ghost_tile256<BK, WAVES, false, true>(E, i, p, q, lds, park, s_lo, s_hi, pa, pa + kG4ParkFloats, 0u, 0u);
       continue;
     }
-    float s = p == q ? ghost_tile256<BK, WAVES, true, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr)
-                     : 2.0f * ghost_tile256<BK, WAVES, false, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr);
+    // Jobs of an example: with halves, diagonal tile k (k < nt), then the two
+    // row halves of every off-diagonal tile; otherwise the tiles of the upper
+    // triangle in row-major order. Columns: diagonal tile p, then a pair per
+    // off-diagonal tile o (one per half; a whole tile writes the second as 0).
+    const int64_t i = w / (uint32_t)E.jpe;
+    const int k = (int)(w % (uint32_t)E.jpe);
+    int half = -1;
+    if (E.halves) {
+      if (k < E.nt) {
+        p = q = k;
+      } else {
+        g4_off_pq(E.nt, (k - E.nt) >> 1, p, q);
+        half = (k - E.nt) & 1;
+      }
+    } else {
+      g4_tile_pq(E.nt, k, p, q);
+    }
+    float s;
+    if (p == q) {
+      s = ghost_tile256<BK, WAVES, true, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr,
+                                                kG4DiagAct, kG4DiagW2);
+    } else {
+      // Half h: the waves of rows 128 h .. +127 of block p (waves 4 h .. 4 h + 3).
+      const uint32_t act = half < 0 ? 0xFFu : 0x0Fu << (4 * half);
+      s = ghost_tile256<BK, WAVES, false, false>(E, i, p, q, lds, park, 0, n, nullptr, nullptr,
+                                                 act, 0xFFu);
+    }
     s = wave_sum(s);
     __syncthreads();   // the ring is free again
     float* red = reinterpret_cast<float*>(lds);
@@ -703,8 +759,19 @@ __global__ __launch_bounds__(64 * WAVES, 1) void ghost_tile256_kernel(G4Args arg
     if (threadIdx.x == 0) {
       float v = 0.f;
 #pragma unroll
-      for (int k = 0; k < WAVES; k += 2) v += red[k] + red[k + 1];
-      args.partials[i * args.P + E.partial_col + pr] = v;
+      for (int k2 = 0; k2 < WAVES; k2 += 2) v += red[k2] + red[k2 + 1];
+      float* col = args.partials + i * args.P + E.partial_col;
+      if (p == q) {
+        col[p] = v;
+      } else {
+        const int c = E.nt + 2 * g4_off_index(E.nt, p, q);
+        if (half < 0) {
+          col[c] = v;
+          col[c + 1] = 0.f;
+        } else {
+          col[c + half] = v;
+        }
+      }
     }
   }
 }
@@ -773,7 +840,14 @@ __global__ __launch_bounds__(kCbThreads) void ghost256_combine_kernel(G4Args arg
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kCbThreads / 64; w += 2) v += red[w] + red[w + 1];
-    args.partials[i * args.P + E.partial_col + pr] = p == q ? v : 2.0f * v;
+    float* col = args.partials + i * args.P + E.partial_col;
+    if (p == q) {
+      col[p] = v;
+    } else {
+      const int c = E.nt + 2 * g4_off_index(E.nt, p, q);
+      col[c] = 2.0f * v;
+      col[c + 1] = 0.f;
+    }
   }
 }
 
@@ -792,35 +866,49 @@ static size_t ghost256_park_floats_per_grid(int64_t jobs) {
   return (size_t)grid * kG4ParkFloats;
 }
 
-int64_t ghost256_pairs(const dpsgd_layer& L) {
+// Tiles of the upper triangle (p <= q) of an example's T x T Gram matrix.
+static int64_t ghost256_pairs(const dpsgd_layer& L) {
   const int64_t nt = ceil_div(L.T, kG4Rows);
   return nt * (nt + 1) / 2;
 }
 
+int64_t ghost256_cols(const dpsgd_layer& L) {
+  const int64_t nt = ceil_div(L.T, kG4Rows);
+  return nt * nt;
+}
+
 namespace {
 
-// Split plan of one launch of 256-row tiles (at most kMaxLayersPerLaunch
-// layers). A job runs on one CU and a tile's time is set by its column
-// slices, so with fewer tiles than CUs the chip idles; splitting every tile's
-// slices into S parts (at least 16 slices each) runs S times as many shorter
-// jobs, at the cost of parking about S + 1 partial Gram tiles per tile for a
-// combine pass. S is the largest (at most 4) whose jobs still fit one round
-// on the CUs: with a second round the per-slice time rises by about a third
-// when every CU copies at once and the parked traffic grows, and the split
-// measured slower (c4's shape, B T = 32768: 0.79 against 0.71 ms), while
-// within one round it measured 1.2-2.6 times faster (B T = 1024 ... 12288).
+// Plan of one launch of 256-row tiles (at most kMaxLayersPerLaunch layers).
+// A job runs on one CU and a tile's time is set by its column slices, so with
+// fewer tiles than CUs the chip idles. Splitting every tile's slices into S
+// parts (at least 16 slices each) runs S times as many shorter jobs, at the
+// cost of parking about S + 1 partial Gram tiles per tile for a combine pass.
+// S is the largest (at most 4) whose jobs still fit one round on the CUs:
+// with a second round the per-slice time rises by about a third when every
+// CU copies at once and the parked traffic grows, and the split measured
+// slower (c4's shape, B T = 32768: 0.79 against 0.71 ms), while within one
+// round it measured 1.2-2.6 times faster (B T = 1024 ... 12288). Without a
+// split, when nt^2 jobs per example (diagonal tiles whole, off-diagonal tiles
+// as two row halves) still fit one round, the halves run: no parked partials
+// and no combine pass (T = 1024, 4096 -> 11008, B = 16: 256 jobs, 0.370-0.375
+// ms against 0.391-0.396 for the 160 whole tiles; T = 512, 768 -> 3072, B =
+// 64: 0.099-0.102 against 0.109-0.116 ms).
 struct G4Plan {
   int split = 1;
+  bool halves = false;
   int64_t tiles = 0;
+  int64_t jobs = 0;
   size_t park_bytes = 0;
 };
 
 G4Plan plan_ghost256(const dpsgd_layer* layers, const int* idx, int n, int64_t cus) {
   G4Plan plan;
-  int64_t slices = 0;
+  int64_t slices = 0, cols = 0;
   for (int k = 0; k < n; ++k) {
     const dpsgd_layer& L = layers[idx[k]];
     plan.tiles += L.B * ghost256_pairs(L);
+    cols += L.B * ghost256_cols(L);
     slices = std::max<int64_t>(slices, (L.d_in + L.d_out) / kG4BK);
   }
   for (int S = 4; S >= 2; --S)
@@ -828,8 +916,10 @@ G4Plan plan_ghost256(const dpsgd_layer* layers, const int* idx, int n, int64_t c
       plan.split = S;
       break;
     }
+  plan.halves = plan.split == 1 && cols > plan.tiles && cols <= cus;
+  plan.jobs = plan.split > 1 ? plan.tiles * plan.split : (plan.halves ? cols : plan.tiles);
   plan.park_bytes = plan.split == 1
-                        ? ghost256_park_floats_per_grid(plan.tiles) * sizeof(float)
+                        ? ghost256_park_floats_per_grid(plan.jobs) * sizeof(float)
                         : (size_t)plan.tiles * plan.split * 2 * kG4ParkFloats * sizeof(float);
   return plan;
 }
@@ -867,10 +957,12 @@ int launch_ghost256(const dpsgd_layer* layers, const int* idx, int n, const int6
       E.T = (int32_t)L.T;
       E.nt = (int32_t)ceil_div(L.T, kG4Rows);
       E.pairs = E.nt * (E.nt + 1) / 2;
+      E.jpe = plan.halves ? E.nt * E.nt : E.pairs;
+      E.halves = plan.halves ? 1 : 0;
       E.partial_col = (int32_t)cols[idx[base + k]];
       E.wg_begin = (uint32_t)jobs;
       a.L[k] = E;
-      jobs += L.B * (int64_t)E.pairs * plan.split;
+      jobs += L.B * (int64_t)(plan.split > 1 ? E.pairs * plan.split : E.jpe);
     }
     if (jobs > 0x7FFFFFFF) return DPSGD_ERR_INVALID_ARG;
     a.jobs = (uint32_t)jobs;

@@ -368,7 +368,7 @@ int64_t norm_partials_per_example(const dpsgd_layer& L, NormForm form) {
   switch (form) {
     case FORM_T1: return 1;
     case FORM_STORED: return skinny_chunks(L);
-    case FORM_GHOST256: return ghost256_pairs(L);
+    case FORM_GHOST256: return ghost256_cols(L);
     case FORM_GHOST: {
       const int64_t nt = ceil_div(L.T, kTile);
       return nt * (nt + 1) / 2;

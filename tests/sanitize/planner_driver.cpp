@@ -82,9 +82,9 @@ int main() {
   // Gram form on 256-row tiles: the park area (256 KB per workgroup) and the
   // grid cap of 512 workgroups (200 x 6 = 1200 jobs).
   const dpsgd_layer c4base = shape(16, 1024, 4096, 11008, BF, 0);
-  CHECK(dpsgd_norms_workspace_bytes(&c4base, 1, DPSGD_NORM_GHOST) >= (size_t)160 * 262144);
+  CHECK(dpsgd_norms_workspace_bytes(&c4base, 1, DPSGD_NORM_GHOST) == 1024 + (size_t)256 * 262144);
   const dpsgd_layer capped = shape(200, 520, 64, 64, BF, 0);
-  CHECK(dpsgd_norms_workspace_bytes(&capped, 1, DPSGD_NORM_GHOST) == 4864 + (size_t)512 * 262144);
+  CHECK(dpsgd_norms_workspace_bytes(&capped, 1, DPSGD_NORM_GHOST) == 7424 + (size_t)512 * 262144);
   queries({capped, shape(200, 300, 128, 64, BF, 1)});
   // Ragged last row tiles of the 384x256 clip kernel, with a split tail, and
   // a 4096 x 4096 layer (one round of 256x256 tiles).

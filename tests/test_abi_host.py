@@ -50,17 +50,19 @@ def test_workspace_queries_and_mode_selection(lib):
     assert dpsgd.dpsgd_select_norm_mode(c3) == dpsgd.DPSGD_NORM_GHOST
     lora = dpsgd.shape_layer(16, 1024, 4096, 16)
     assert dpsgd.dpsgd_select_norm_mode(lora) == dpsgd.DPSGD_NORM_MATERIALIZE
-    # T = 512 bf16 runs the Gram form on 256-row tiles: 3 upper-triangle tile
-    # pairs per example (partials 64 x 3 floats, rounded to 256 bytes), then a
-    # 256 KB float32 park slot per workgroup of the 192-job grid.
-    assert dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 768 + 192 * 262144
+    # T = 512 bf16 runs the Gram form on 256-row tiles: 2 row blocks, so 4
+    # partials per example (one per diagonal tile, two per off-diagonal tile;
+    # 64 x 4 floats), and the 192 tiles become 256 jobs (the off-diagonal
+    # tiles as two row halves), each workgroup with a 256 KB float32 park slot.
+    assert dpsgd.dpsgd_norms_workspace_bytes(c3, dpsgd.DPSGD_NORM_GHOST) == 1024 + 256 * 262144
     # More than 512 jobs: the grid (and the park area) stays at 512 workgroups.
-    big = dpsgd.shape_layer(200, 520, 64, 64)    # 3 row blocks, 6 pairs, 1200 jobs
-    assert dpsgd.dpsgd_norms_workspace_bytes(big, dpsgd.DPSGD_NORM_GHOST) == 4864 + 512 * 262144
-    # c4's 11008-wide layer: 160 tiles of 236 column slices; splitting them
-    # would need a second round on 256 CUs, so they stay whole.
+    big = dpsgd.shape_layer(200, 520, 64, 64)    # 3 row blocks, 6 tiles, 1200 jobs
+    assert dpsgd.dpsgd_norms_workspace_bytes(big, dpsgd.DPSGD_NORM_GHOST) == 7424 + 512 * 262144
+    # c4's 11008-wide layer: 160 tiles of 236 column slices; splitting their
+    # columns would need a second round on 256 CUs, while 4 + 2 x 6 = 16 jobs
+    # per example (256) fill exactly one.
     c4 = dpsgd.shape_layer(16, 1024, 4096, 11008)
-    assert dpsgd.dpsgd_norms_workspace_bytes(c4, dpsgd.DPSGD_NORM_GHOST) == 768 + 160 * 262144
+    assert dpsgd.dpsgd_norms_workspace_bytes(c4, dpsgd.DPSGD_NORM_GHOST) == 1024 + 256 * 262144
     # At B = 8 (80 tiles) each tile is split into 3 column parts (240 jobs, one
     # round) that park their partial Gram tiles: two 256 KB slots per part.
     c4b8 = dpsgd.shape_layer(8, 1024, 4096, 11008)

@@ -2,13 +2,16 @@
 
 Per-example squared norms ||G_i^T A_i||_F^2 (Section 2.2's clipping norm) of
 bf16 layers with T > 256 run one 256 x 256 tile of the T x T upper triangle
-per workgroup, parking the activation Gram tile in the workspace; with few
-tiles and long rows every tile's columns are split into parts whose partial
-Gram tiles a combine pass adds. Cases: layers of different T in one launch,
-split tiles (a part with only A's columns, a part across the A/G boundary),
-more jobs than the capped grid (workgroups take several jobs and reuse their
-park slot), the fused clipped-sum call, and agreement with the 128-row-tile
-kernel of the allocation-free call.
+per workgroup (a diagonal tile skips its sub-tiles below the 128-row
+diagonal), parking the activation Gram tile in the workspace; when the tiles
+fill fewer than the CUs, the off-diagonal tiles run as two row halves, or,
+with few tiles and long rows, every tile's columns are split into parts
+whose partial Gram tiles a combine pass adds. Cases: layers of different T
+in one launch (row halves), split tiles (a part with only A's columns, a
+part across the A/G boundary, empty parts), more jobs than the capped grid
+(whole tiles; workgroups take several jobs and reuse their park slot), the
+fused clipped-sum call, and agreement with the 128-row-tile kernel of the
+allocation-free call.
 """
 
 import sys

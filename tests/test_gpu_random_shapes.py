@@ -2,8 +2,10 @@
 float64 oracle.
 
 Each case draws layer shapes that the library's rules route to one path: the
-Gram form on three-tile groups (128 < T <= 256), on whole 256-row tiles and on
-256-row tiles split along the columns (T > 256); the clip-weighted sum on
+Gram form on three-tile groups (128 < T <= 256), and for T > 256 on 256-row
+tiles with the off-diagonal tiles as two row halves, on whole 256-row tiles
+(more jobs than CUs) and on 256-row tiles split along the columns; the
+clip-weighted sum on
 whole 384 x 256 tiles, on a ragged last row of 384 x 256 tiles, on 256 x 256
 tiles and on the 128-tile kernel. The step runs through the C ABI (norms,
 clip factors, clipped sums, Philox noise; Section 2.2 and the GPU-side
@@ -42,10 +44,14 @@ def _case(kind, seed):
         B = int(rng.integers(2, 5))
         return B, [(int(rng.integers(129, 257)), _m(rng, 64, 512, 64), _m(rng, 64, 512, 64))
                    for _ in range(2)]
-    if kind == "gram 256-row tiles":
+    if kind == "gram row halves":
         B = int(rng.integers(2, 5))
         return B, [(int(rng.integers(257, 1100)), _m(rng, 64, 448, 64), _m(rng, 64, 448, 64))
                    for _ in range(2)]
+    if kind == "gram whole 256-row tiles":
+        # 4 row blocks, more than 256 CUs' worth of half jobs (B 4^2 > 256).
+        B = int(rng.integers(17, 21))
+        return B, [(int(rng.integers(769, 1025)), _m(rng, 64, 192, 64), _m(rng, 64, 192, 64))]
     if kind == "gram split tiles":
         # Few tiles, at least 32 column slices: every tile split into parts.
         return 1, [(int(rng.integers(257, 900)), _m(rng, 1024, 1536, 64), _m(rng, 1024, 1536, 64))]
@@ -69,18 +75,37 @@ def _case(kind, seed):
     raise ValueError(kind)
 
 
-KINDS = ["gram groups", "gram 256-row tiles", "gram split tiles", "clip 384x256",
+KINDS = ["gram groups", "gram row halves", "gram whole 256-row tiles", "gram split tiles",
+         "clip 384x256",
          "clip ragged 384x256", "clip 256x256", "clip 128-tile"]
-CASES = [(k, 7000 + 13 * i) for i, k in enumerate(KINDS)] + [("gram 256-row tiles", 7200),
+CASES = [(k, 7000 + 13 * i) for i, k in enumerate(KINDS)] + [("gram row halves", 7200),
                                                             ("clip 384x256", 7300)]
+
+
+def _gram256_mode(B, dims):
+    """Job mode of one launch of 256-row tiles (the planner's rule restated):
+    a column split into S parts when S times the tiles fit 256 CUs with parts
+    of at least 16 slices, else row halves when B nt^2 jobs fit, else whole."""
+    nts = [-(-T // 256) for T, _, _ in dims]
+    tiles = sum(B * nt * (nt + 1) // 2 for nt in nts)
+    jobs = sum(B * nt * nt for nt in nts)
+    slices = max((d_in + d_out) // 64 for _, d_in, d_out in dims)
+    for S in (4, 3, 2):
+        if tiles * S <= 256 and slices // S >= 16:
+            return "split"
+    return "halves" if tiles < jobs <= 256 else "whole"
 
 
 def _check_route(kind, B, dims):
     """The drawn shapes take the intended path (the library's rules restated)."""
+    if kind.startswith("gram") and kind != "gram groups":
+        want = {"gram row halves": "halves", "gram whole 256-row tiles": "whole",
+                "gram split tiles": "split"}[kind]
+        assert _gram256_mode(B, dims) == want, (kind, B, dims)
     for T, d_in, d_out in dims:
         if kind == "gram groups":
             assert 128 < T <= 256 and d_in % 64 == 0 and d_out % 64 == 0
-        elif kind == "gram 256-row tiles":
+        elif kind in ("gram row halves", "gram whole 256-row tiles"):
             assert T > 256 and (d_in + d_out) // 64 < 32
         elif kind == "gram split tiles":
             nt = -(-T // 256)

@@ -396,7 +396,9 @@ def g4_gram(bk, waves, X, T, p, q):
     return acc
 
 
-def g4_tile_sum(bk, waves, A, G, T, p, q):
+def g4_wave_sums(bk, waves, A, G, T, p, q):
+    """Each wave's masked sum of GA * GG over its sub-tile of tile (p, q),
+    through the park slots (every slot written once, read back by its lane)."""
     GA = g4_gram(bk, waves, A, T, p, q)
     GG = g4_gram(bk, waves, G, T, p, q)
     mb, nb = 16 // waves, 4
@@ -408,8 +410,9 @@ def g4_tile_sum(bk, waves, A, G, T, p, q):
     # Lane l, element v: block row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32.
     br = 8 * (v[None, :] >> 2) + 4 * (lane[:, None] >> 5) + (v[None, :] & 3)
     bc = np.broadcast_to(lane[:, None] & 31, br.shape)
-    total = 0.0
+    sums = {}
     for wave in range(waves):
+        total = 0.0
         wm, wn = wave >> 1, wave & 1
         for a in range(mb):
             for b in range(nb):
@@ -426,8 +429,13 @@ def g4_tile_sum(bk, waves, A, G, T, p, q):
                 col = 32 * (nb * wn + b) + bc
                 mask = (row < rows_p) & (col < rows_q)
                 total += float(np.sum(np.where(mask, back * GG[(wave, a, b)][br, bc], 0.0)))
+        sums[wave] = total
     assert not np.any(np.isnan(park)), "park slot never written"
-    return total
+    return sums
+
+
+def g4_tile_sum(bk, waves, A, G, T, p, q):
+    return sum(g4_wave_sums(bk, waves, A, G, T, p, q).values())
 
 
 @pytest.mark.parametrize("bk,waves", [(64, 8), (64, 4), (32, 8)])
@@ -453,6 +461,96 @@ def test_ghost256_tiles_give_the_norm(bk, waves, T, d_in, d_out):
     assert len(seen) == nt * (nt + 1) // 2
     want = float(np.sum((G.T @ A) ** 2))
     assert total == pytest.approx(want, rel=1e-12)
+
+
+# Jobs of one example without a column split (ghost_tile256_kernel): with
+# halves, diagonal tile k for k < nt, then the two 128-row halves of every
+# off-diagonal tile o (row-major over p < q); otherwise the upper-triangle
+# tiles in row-major order. Eight waves; a diagonal tile skips waves 4 and 6
+# (the sub-tiles below its 128-row diagonal) and weights waves 1 and 3 by 2;
+# an off-diagonal tile weights every wave by 2, and half h keeps waves
+# 4 h .. 4 h + 3. Partial columns: diagonal tile p, then nt + 2 o + h.
+G4_DIAG_ACT, G4_DIAG_W2 = 0xAF, 0x0A
+
+
+def g4_off_pq(nt, o):
+    p = 0
+    while o >= nt - 1 - p:
+        o -= nt - 1 - p
+        p += 1
+    return p, p + 1 + o
+
+
+def g4_off_index(nt, p, q):
+    return p * (nt - 1) - p * (p - 1) // 2 + (q - p - 1)
+
+
+def g4_jobs(nt, halves):
+    """(p, q, act, w2, columns written) per job of one example."""
+    out = []
+    for k in range(nt * nt if halves else nt * (nt + 1) // 2):
+        half = -1
+        if halves and k < nt:
+            p = q = k
+        elif halves:
+            p, q = g4_off_pq(nt, (k - nt) >> 1)
+            half = (k - nt) & 1
+        else:
+            pr, p = k, 0
+            while pr >= nt - p:
+                pr -= nt - p
+                p += 1
+            q = p + pr
+        if p == q:
+            out.append((p, q, G4_DIAG_ACT, G4_DIAG_W2, [p]))
+            continue
+        c = nt + 2 * g4_off_index(nt, p, q)
+        act = 0xFF if half < 0 else 0x0F << (4 * half)
+        out.append((p, q, act, 0xFF, [c, c + 1] if half < 0 else [c + half]))
+    return out
+
+
+@pytest.mark.parametrize("nt", range(1, 9))
+@pytest.mark.parametrize("halves", [False, True])
+def test_ghost256_jobs_weight_every_entry_once(nt, halves):
+    """The active sub-tiles' weights, added to their mirror images, count every
+    entry of the symmetric T x T product once, and every partial column is
+    written by exactly one job."""
+    T = 256 * nt
+    weight = np.zeros((T, T))
+    cols = np.zeros(nt * nt, int)
+    for p, q, act, w2, written in g4_jobs(nt, halves):
+        for wave in range(8):
+            if (act >> wave) & 1:
+                wm, wn = wave >> 1, wave & 1
+                r0, c0 = 256 * p + 64 * wm, 256 * q + 128 * wn
+                weight[r0:r0 + 64, c0:c0 + 128] += 2.0 if (w2 >> wave) & 1 else 1.0
+        for c in written:
+            cols[c] += 1
+    assert np.all(weight + weight.T == 2.0)
+    assert np.all(cols == 1)
+    for o in range(nt * (nt - 1) // 2):
+        p, q = g4_off_pq(nt, o)
+        assert p < q < nt and g4_off_index(nt, p, q) == o
+
+
+@pytest.mark.parametrize("halves", [False, True])
+@pytest.mark.parametrize("T,d_in,d_out", [(300, 64, 128), (520, 128, 64), (777, 64, 64)])
+def test_ghost256_job_decode_gives_the_norm(halves, T, d_in, d_out):
+    """Wave sums of the modelled kernel, kept by the job's masks and weights,
+    add up to ||G^T A||^2 on ragged T (rows past T masked out)."""
+    rng = np.random.default_rng(T + d_in + (7 if halves else 0))
+    A = rng.integers(-3, 4, (T, d_in)).astype(np.float64)
+    G = rng.integers(-3, 4, (T, d_out)).astype(np.float64)
+    nt = -(-T // 256)
+    cache, total = {}, 0.0
+    for p, q, act, w2, _ in g4_jobs(nt, halves):
+        if (p, q) not in cache:
+            cache[(p, q)] = g4_wave_sums(64, 8, A, G, T, p, q)
+        for wave, ws in cache[(p, q)].items():
+            if (act >> wave) & 1:
+                total += (2.0 if (w2 >> wave) & 1 else 1.0) * ws
+    assert total == pytest.approx(float(np.sum((G.T @ A) ** 2)), rel=1e-12)
 
 
 @pytest.mark.parametrize("jobs", [1, 7, 160, 192, 511, 512, 513, 1080, 4099])
