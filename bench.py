@@ -74,8 +74,8 @@ def parse():
                         "adapter layers read once); the norms then have no time of their own")
     p.add_argument("--cpu-sample-examples", type=int, default=40)
     p.add_argument("--pmc-probe", action="store_true",
-                   help="run a 1 GiB copy and one call of each entry point, then exit "
-                        "(for rocprofv3 counter passes)")
+                   help="run a 1 GiB copy and one call of each entry point (with --fused also "
+                        "the one-call form), then exit (for rocprofv3 counter passes)")
     return p.parse_args()
 
 
@@ -271,6 +271,11 @@ def main():
                                             workspace=buf.norms_ws)
         dpsgd.dpsgd_clip_accumulate_multi(Ls, buf.norms_sq, W.C, buf.grads, workspace=buf.clip_ws)
         dpsgd.dpsgd_add_noise_multi(Ls, buf.grads, W.sigma, W.C, W.noise_seed, W.step, scale)
+        if args.fused:
+            # The one-call form too (its stored-gradient kernels for adapter layers).
+            dpsgd.dpsgd_clipped_sum_multi(Ls, dpsgd.DPSGD_NORM_AUTO, W.C, buf.grads, buf.norms_sq,
+                                          factors_out=buf.factors, mask_out=buf.mask,
+                                          workspace=buf.fused_ws)
         params = [torch.randn_like(g) for g in buf.grads]
         moms = [torch.zeros_like(g) for g in buf.grads]
         moms2 = [torch.zeros_like(g) for g in buf.grads]
