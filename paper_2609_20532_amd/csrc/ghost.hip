@@ -475,11 +475,13 @@ struct G4Args {
   float* park;
 };
 
-// sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] of 256 x 256 tile (p, q) of example
-// i over the column slices [s_lo, s_hi) (A's slices first, then G's), with
-// park a kG4ParkFloats scratch slot of this workgroup. SPLIT: the slices are
-// part of the tile; the partial GA (masked) goes to park_a and the partial GG
-// to park_g instead, and the result is 0.
+// This wave's part of sum_{t<rows_p, s<rows_q} GA[t][s] GG[t][s] over 256 x 256
+// tile (p, q) of example i: the sum over its sub-tile, doubled when the wave
+// is in w2_mask, 0 when it is not in act_mask; park is a kG4ParkFloats scratch
+// slot of this workgroup. SPLIT: the column slices [s_lo, s_hi) (A's slices
+// first, then G's) are part of the tile and every wave takes part; the
+// partial GA (masked) goes to park_a and the partial GG to park_g instead,
+// and the result is 0.
 template <int BK, int WAVES, bool DIAG, bool SPLIT>
 __device__ float ghost_tile256(const GhEntry& E, int64_t i, int p, int q, char* lds, float* park,
                                int s_lo_arg, int s_hi_arg, float* park_a, float* park_g,
