@@ -73,6 +73,11 @@ CASES = [
     # One launch split in 4 parts for the large layer; the small layer's 2
     # slices leave two of its parts empty.
     (1, [(512, 2048, 2048), (300, 64, 64)]),
+    # Long sequences: 8 and 12 (ragged) row blocks as row halves, and 12 row
+    # blocks at B = 4 as whole tiles (312 tiles, 576 half jobs > 256 CUs).
+    (2, [(2048, 64, 64)]),
+    (1, [(3000, 128, 64)]),
+    (4, [(3000, 64, 64)]),
 ]
 
 
