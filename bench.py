@@ -73,6 +73,9 @@ def parse():
                    help="run norms + clipped sum as one dpsgd_clipped_sum_multi call (low-rank "
                         "adapter layers read once); the norms then have no time of their own")
     p.add_argument("--cpu-sample-examples", type=int, default=40)
+    p.add_argument("--vendor-reference", action="store_true",
+                   help="time the platform BLAS (torch.mm, bf16) on the workload's layer products "
+                        "without clip weights and on square products, print one JSON line, exit")
     p.add_argument("--pmc-probe", action="store_true",
                    help="run a 1 GiB copy and one call of each entry point (with --fused also "
                         "the one-call form), then exit (for rocprofv3 counter passes)")
@@ -231,6 +234,46 @@ def time_noise_adamw(dpsgd, Ls, buf, W, scale, steps):
     return t
 
 
+def vendor_reference(W, layers_t, dev, reps: int = 20):
+    """The platform BLAS on the same contractions, for scale: sum_k G[k]^T A[k]
+    of every layer (one torch.mm per layer, K = B T, no clip weights, G^T made
+    contiguous beforehand) and square bf16 products of N(0, 1) data."""
+    import torch
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    K = W.B * W.T
+    ops = []
+    for d in layers_t:
+        Gt = d["G"].reshape(K, -1).t().contiguous()          # [d_out, K]
+        A = d["A"].reshape(K, -1).contiguous()               # [K, d_in]
+        ops.append((Gt, A))
+    flops = sum(2.0 * K * Gt.shape[0] * A.shape[1] for Gt, A in ops)
+    ms = timed(lambda: [torch.mm(Gt, A) for Gt, A in ops])
+    out = {"vendor_reference": W.name, "layer_products_ms": ms,
+           "layer_products_tflops": flops / ms / 1e9, "square": {}}
+    del ops
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    for n in (4096, 8192, 16384):
+        X = torch.randn(n, n, generator=g, device=dev).to(torch.bfloat16)
+        Y = torch.randn(n, n, generator=g, device=dev).to(torch.bfloat16)
+        t = timed(lambda: torch.mm(X, Y))
+        out["square"][str(n)] = {"ms": t, "tflops": 2.0 * n ** 3 / t / 1e9}
+        del X, Y
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -259,6 +302,10 @@ def main():
     work = algorithmic_work(W, forms)
     scale = 1.0 / W.B
     torch.cuda.synchronize()
+
+    if args.vendor_reference:
+        print(json.dumps(vendor_reference(W, layers_t, dev)), flush=True)
+        return
 
     if args.pmc_probe:
         # Calibration copy of known size, then one launch of each entry point.
