@@ -7,7 +7,8 @@ tiles with the off-diagonal tiles as two row halves, on whole 256-row tiles
 (more jobs than CUs) and on 256-row tiles split along the columns; the
 clip-weighted sum on
 whole 384 x 256 tiles, on a ragged last row of 384 x 256 tiles, on 256 x 256
-tiles and on the 128-tile kernel. The step runs through the C ABI (norms,
+tiles and on the 128-tile kernel, and steps that mix layers of several of
+these paths in one call. The step runs through the C ABI (norms,
 clip factors, clipped sums, Philox noise; Section 2.2 and the GPU-side
 algorithm) and is checked before and after the noise as the other step tests
 do. The shapes are drawn from fixed seeds, so every run checks the same ones.
@@ -72,14 +73,23 @@ def _case(kind, seed):
         B = int(rng.integers(2, 5))
         return B, [(int(rng.integers(40, 200)), int(rng.integers(20, 300)),
                     int(rng.integers(20, 300)))]
+    if kind == "mixed":
+        # Layers drawn for two to four of the paths above in one step (B = 2):
+        # one call then runs several kernel kinds side by side.
+        picks = rng.choice(len(KINDS), size=int(rng.integers(2, 5)), replace=False)
+        dims = []
+        for k in picks:
+            dims += _case(KINDS[int(k)], int(rng.integers(1, 10 ** 6)))[1]
+        return 2, dims
     raise ValueError(kind)
 
 
 KINDS = ["gram groups", "gram row halves", "gram whole 256-row tiles", "gram split tiles",
          "clip 384x256",
          "clip ragged 384x256", "clip 256x256", "clip 128-tile"]
-CASES = [(k, 7000 + 13 * i) for i, k in enumerate(KINDS)] + [("gram row halves", 7200),
-                                                            ("clip 384x256", 7300)]
+CASES = ([(k, 7000 + 13 * i) for i, k in enumerate(KINDS)]
+         + [("mixed", 7400 + j) for j in range(3)]
+         + [("gram row halves", 7200), ("clip 384x256", 7300)])
 
 
 def _gram256_mode(B, dims):
@@ -98,6 +108,8 @@ def _gram256_mode(B, dims):
 
 def _check_route(kind, B, dims):
     """The drawn shapes take the intended path (the library's rules restated)."""
+    if kind == "mixed":
+        return
     if kind.startswith("gram") and kind != "gram groups":
         want = {"gram row halves": "halves", "gram whole 256-row tiles": "whole",
                 "gram split tiles": "split"}[kind]
